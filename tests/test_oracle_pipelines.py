@@ -1,0 +1,149 @@
+"""Pins for the oracle's pipeline compositions and for the input generator.
+
+The pipelines only compose pinned operators with bf16 rounding at operator
+boundaries; these tests check the composition itself (explicit step-by-step
+recomputation, row subsets equal to the full result) on shrunken workloads
+with the same structure as the benchmark ones.
+"""
+
+from types import SimpleNamespace
+
+import numpy as np
+import pytest
+
+from oracle import ikbo, pipelines
+from oracle.bf16 import round_bf16
+from paper_2607_27744_amd import workloads as wl
+
+
+def _small3():
+    counts, lens = np.array([3, 5, 1, 4]), np.array([7, 2, 9, 5])
+    rng = lambda t: wl.tensor_rng(0, 33, t)  # noqa: E731
+    ns = SimpleNamespace(n_req=4, n_cand=13, n_heads=2, head_dim=4,
+                         cand_offsets=wl.offsets_from_counts(counts),
+                         kv_offsets=wl.offsets_from_counts(lens),
+                         e_c=wl.normal(rng(1), (13, 8)), s=wl.normal(rng(2), (23, 8)))
+    for layer in (1, 2):
+        for j, name in enumerate(("wq", "wk", "wv")):
+            setattr(ns, f"{name}{layer}", wl.normal(rng(10 * layer + j), (8, 8), std=0.35))
+    return ns
+
+
+def test_ranking_pipeline_composition_and_rows():
+    w = _small3()
+    out = pipelines.ranking_dca(w)
+    k1 = round_bf16(ikbo.sequence_projection(w.s, w.wk1))
+    v1 = round_bf16(ikbo.sequence_projection(w.s, w.wv1))
+    q1 = round_bf16(ikbo.linear(w.e_c, w.wq1))
+    a1 = round_bf16(ikbo.dca_attention(q1.reshape(13, 1, 2, 4), k1.reshape(23, 2, 4),
+                                       v1.reshape(23, 2, 4), w.cand_offsets, w.kv_offsets,
+                                       mode="explicit").reshape(13, 8))
+    np.testing.assert_array_equal(out["a1"], a1)
+    u = round_bf16(a1 + w.e_c)
+    q2 = round_bf16(ikbo.linear(u, w.wq2))
+    k2 = round_bf16(ikbo.sequence_projection(w.s, w.wk2))
+    v2 = round_bf16(ikbo.sequence_projection(w.s, w.wv2))
+    a2 = round_bf16(ikbo.dca_attention(q2.reshape(13, 1, 2, 4), k2.reshape(23, 2, 4),
+                                       v2.reshape(23, 2, 4), w.cand_offsets, w.kv_offsets,
+                                       mode="explicit").reshape(13, 8))
+    np.testing.assert_array_equal(out["a2"], a2)
+    rows = np.array([12, 0, 7])
+    sub = pipelines.ranking_dca(w, rows=rows)
+    np.testing.assert_array_equal(sub["a2"], a2[rows])
+
+
+def _small5():
+    counts = np.array([6, 0, 9])
+    rng = lambda t: wl.tensor_rng(0, 55, t)  # noqa: E731
+    return SimpleNamespace(
+        n_req=3, n_cand=15, n_heads=2, head_dim=4,
+        cand_offsets=wl.offsets_from_counts(counts),
+        kv_offsets=wl.offsets_from_counts([5, 3, 8]),
+        x_req=wl.normal(rng(1), (3, 12)), x_cand=wl.normal(rng(2), (15, 4)),
+        w1_req=wl.normal(rng(3), (8, 12), std=0.25), w1_cand=wl.normal(rng(4), (8, 4), std=0.25),
+        w2=wl.normal(rng(5), (3, 8), std=0.35), s=wl.normal(rng(6), (16, 5)),
+        wk=wl.normal(rng(7), (8, 5), std=0.45), wv=wl.normal(rng(8), (8, 5), std=0.45))
+
+
+def test_production_pipeline_composition_and_rows():
+    w = _small5()
+    out = pipelines.production_retrieval(w)
+    h1 = round_bf16(ikbo.ikbo_linear_decomposed(w.x_req, w.x_cand, w.w1_req, w.w1_cand,
+                                                None, w.cand_offsets, "relu"))
+    np.testing.assert_allclose(out["h1"], h1, rtol=0, atol=0)
+    np.testing.assert_array_equal(out["out2"], round_bf16(h1 @ np.asarray(w.w2, np.float64).T))
+    k = round_bf16(np.asarray(w.s, np.float64) @ np.asarray(w.wk, np.float64).T)
+    v = round_bf16(np.asarray(w.s, np.float64) @ np.asarray(w.wv, np.float64).T)
+    att = round_bf16(ikbo.dca_attention(h1.reshape(15, 1, 2, 4), k.reshape(16, 2, 4),
+                                        v.reshape(16, 2, 4), w.cand_offsets, w.kv_offsets,
+                                        mode="explicit").reshape(15, 8))
+    np.testing.assert_array_equal(out["attention"], att)
+    rows = np.array([14, 3, 6])
+    sub = pipelines.production_retrieval(w, rows=rows)
+    for key in ("h1", "out2", "attention"):
+        np.testing.assert_array_equal(sub[key], out[key][rows])
+
+
+def test_fm_pipeline_rows():
+    rng = lambda t: wl.tensor_rng(0, 44, t)  # noqa: E731
+    w = SimpleNamespace(n_req=2, n_cand=7, cand_offsets=wl.offsets_from_counts([4, 3]),
+                        x_req=wl.normal(rng(1), (2, 3, 6)), x_cand=wl.normal(rng(2), (7, 2, 6)),
+                        w_req=wl.normal(rng(3), (5, 9), std=0.3),
+                        w_cand=wl.normal(rng(4), (5, 10), std=0.3))
+    full = pipelines.fm_linear(w)
+    y_req, y_cand = ikbo.glm_fm(w.x_req, w.x_cand, w.cand_offsets)
+    want = round_bf16(ikbo.ikbo_linear(round_bf16(y_req), round_bf16(y_cand), w.w_req,
+                                       w.w_cand, None, w.cand_offsets, "relu"))
+    np.testing.assert_array_equal(full["out"], want)
+    rows = np.array([6, 1])
+    np.testing.assert_array_equal(pipelines.fm_linear(w, rows=rows)["out"], want[rows])
+
+
+def test_retrieval_pipeline_rows():
+    w = SimpleNamespace(**vars(_small5()))
+    full = pipelines.retrieval_mlp(w)
+    rows = np.array([2, 9])
+    sub = pipelines.retrieval_mlp(w, rows=rows)
+    np.testing.assert_array_equal(sub["out"], full["out"][rows])
+
+
+# ---------------------------------------------------------------------------
+# Generator
+# ---------------------------------------------------------------------------
+
+def test_generator_deterministic_and_on_bf16_grid():
+    a = wl.linear_case([3, 4], 16, 8, 12, seed=5)
+    b = wl.linear_case([3, 4], 16, 8, 12, seed=5)
+    c = wl.linear_case([3, 4], 16, 8, 12, seed=6)
+    np.testing.assert_array_equal(a.x_cand, b.x_cand)
+    assert not np.array_equal(a.x_cand, c.x_cand)
+    from oracle.bf16 import is_bf16_representable
+    for arr in (a.x_req, a.x_cand, a.w_req, a.w_cand):
+        assert is_bf16_representable(arr).all()
+    np.testing.assert_array_equal(a.cand_offsets, [0, 3, 7])
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4])
+def test_workload_shapes_and_distributions(cid):
+    w = wl.make_workload(cid)
+    off = ikbo.check_offsets(w.cand_offsets, w.n_cand)
+    counts = np.diff(off)
+    if cid == 1:
+        assert w.n_cand == 256 and w.x_req.shape == (4, 256) and w.w_req.shape == (256, 256)
+        assert w.q.shape == (256, 1, 2, 32) and w.k.shape == (128, 2, 32)
+        assert w.x_req.dtype == np.float32
+    if cid == 2:
+        assert counts.min() >= 512 and counts.max() <= 1536 and abs(w.n_cand - 65536) < 6000
+        assert w.w1_req.shape == (512, 1024) and w.w1_cand.shape == (512, 256)
+        std = np.concatenate([w.w1_req.ravel(), w.w1_cand.ravel()]).std()
+        assert abs(std - 1 / np.sqrt(1280)) < 0.02 / np.sqrt(1280)
+    if cid == 3:
+        lens = np.diff(w.kv_offsets)
+        assert counts.min() >= 16 and counts.max() <= 1024 and abs(counts.mean() - 200) < 5
+        assert lens.min() >= 256 and lens.max() <= 1024
+        assert w.s.shape == (lens.sum(), 256) and w.wq1.shape == (256, 256)
+    if cid == 4:
+        assert w.x_req.shape == (128, 32, 128) and w.x_cand.shape == (65536, 8, 128)
+        assert w.w_req.shape == (512, 1024) and w.w_cand.shape == (512, 320)
+    feats = w.e_c if cid == 3 else w.x_cand
+    assert abs(float(np.mean(feats))) < 0.01 and abs(float(np.std(feats)) - 1) < 0.01
