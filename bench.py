@@ -1,0 +1,284 @@
+"""Throughput benchmark of the IKBO hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 5] [--no-cpu-baseline]
+
+A step is one pass of the workload's whole hot path over one batch (default:
+workload 5, production-scale retrieval: 16 requests x 65,536 candidates; IKBO
+linear 2048+512 -> 1024 with ReLU, linear 1024 -> 256, request-side K/V
+projection of the 2048-row histories, DCA attention with 8 heads x 128). Inputs
+and weights are resident in HBM before timing starts; W untimed steps, then K
+timed steps between device synchronisations. Prints ONE JSON line.
+
+roofline: the kernel with the largest time per step, timed live with HIP
+events recorded on the stream it runs on, against its algorithmic FLOPs (or
+bytes) per launch. cpu_baseline: the CPU oracle, timed on this host on a
+bounded sample of the same workload.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+_ROOT = os.path.dirname(os.path.abspath(__file__))
+if _ROOT not in sys.path:
+    sys.path.insert(0, _ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# Algorithmic work per operator call: FLOPs the operator must do (request
+# work once per request, candidate work once per candidate) and bytes it must
+# move (each tensor read or written once). The avoided broadcast is not
+# counted.
+# ---------------------------------------------------------------------------
+
+def _linear_work(n_req, n_cand, k_req, k_cand, d_out, esize=2, add=False):
+    flops = 2.0 * n_cand * k_cand * d_out + 2.0 * n_req * k_req * d_out
+    byts = esize * (n_cand * k_cand * (2 if add else 1) + n_cand * d_out
+                    + (k_req + k_cand) * d_out + n_req * k_req)
+    return flops, byts
+
+
+def _attention_work(n_cand, q_len, heads, dim, kv_lens, esize=2):
+    pairs = 0.0
+    for n_r, l_r in kv_lens:
+        pairs += n_r * q_len * l_r
+    flops = 4.0 * pairs * heads * dim
+    total_l = sum(l for _, l in kv_lens)
+    byts = esize * (2 * n_cand * q_len * heads * dim + 2 * total_l * heads * dim)
+    return flops, byts
+
+
+def _fm_work(n_req, n_cand, f_req, f_cand, emb, esize=2):
+    flops = 2.0 * n_cand * f_cand * (f_req + f_cand) * emb + 2.0 * n_req * f_req * f_req * emb
+    byts = esize * (n_cand * f_cand * emb + n_req * f_req * emb
+                    + n_cand * f_cand * (f_req + f_cand) + n_req * f_req * f_req)
+    return flops, byts
+
+
+def op_plan(w):
+    """[(name, flops, bytes, bound)] for one step, in launch order."""
+    import numpy as np
+    counts = np.diff(np.asarray(w.cand_offsets, dtype=np.int64))
+    cid = w.config_id
+    if cid == 1:
+        return [("ikbo_linear", *_linear_work(4, 256, 256, 128, 256, 4), "alu"),
+                ("dca_attention", *_attention_work(256, 1, 2, 32, [(64, 32)] * 4, 4), "alu")]
+    if cid == 2:
+        return [("ikbo_linear_l1", *_linear_work(w.n_req, w.n_cand, 1024, 256, 512), "hbm"),
+                ("linear_l2", *_linear_work(0, w.n_cand, 0, 512, 256), "hbm")]
+    if cid == 3:
+        lens = np.diff(np.asarray(w.kv_offsets, dtype=np.int64))
+        l_tot = int(lens.sum())
+        att = _attention_work(w.n_cand, 1, 4, 64, list(zip(counts, lens)))
+        kv = _linear_work(0, l_tot, 0, 256, 512)
+        q = _linear_work(0, w.n_cand, 0, 256, 256)
+        q2 = _linear_work(0, w.n_cand, 0, 256, 256, add=True)
+        return [("kv_projection_l1", *kv, "hbm"), ("q_projection_l1", *q, "hbm"),
+                ("dca_attention_l1", *att, "hbm"), ("kv_projection_l2", *kv, "hbm"),
+                ("q_projection_l2", *q2, "hbm"), ("dca_attention_l2", *att, "hbm")]
+    if cid == 4:
+        return [("glm_interaction", *_fm_work(w.n_req, w.n_cand, 32, 8, 128), "hbm"),
+                ("ikbo_linear", *_linear_work(w.n_req, w.n_cand, 1024, 320, 512), "hbm")]
+    if cid == 5:
+        lens = np.diff(np.asarray(w.kv_offsets, dtype=np.int64))
+        return [("ikbo_linear_l1", *_linear_work(w.n_req, w.n_cand, 2048, 512, 1024), "mfma"),
+                ("linear_l2", *_linear_work(0, w.n_cand, 0, 1024, 256), "hbm"),
+                ("kv_projection", *_linear_work(0, int(lens.sum()), 0, 1024, 2048), "mfma"),
+                ("dca_attention", *_attention_work(w.n_cand, 1, 8, 128,
+                                                   list(zip(counts, lens))), "mfma")]
+    raise ValueError(cid)
+
+
+def timed_step_fns(p):
+    """The step split into its operator calls (same calls as pipelines.step)."""
+    from paper_2607_27744_amd import ops, pipelines
+    cid = p.config_id
+    n = p.n_cand
+    kvv = pipelines._kv_views
+    if cid == 1:
+        return [lambda: ops.ikbo_linear(p.x_cand, p.w_cand, x_req=p.x_req, w_req=p.w_req,
+                                        cand_offsets=p.cand_offsets, activation="relu",
+                                        out=p.linear, workspace=p.ws),
+                lambda: ops.dca_attention(p.q, p.k, p.v, p.cand_offsets, p.kv_offsets,
+                                          out=p.attention)]
+    if cid == 2:
+        return [lambda: ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
+                                        cand_offsets=p.cand_offsets, activation="relu",
+                                        out=p.h1, workspace=p.ws),
+                lambda: ops.ikbo_linear(p.h1, p.w2, out=p.out)]
+    if cid == 3:
+        def att(q, kv, o):
+            k, v = kvv(kv, p.h, p.d)
+            return ops.dca_attention(q.view(n, 1, p.h, p.d), k, v, p.cand_offsets,
+                                     p.kv_offsets, out=o)
+        return [lambda: ops.ikbo_linear(p.s, p.wkv1, out=p.kv1),
+                lambda: ops.ikbo_linear(p.e_c, p.wq1, out=p.q1),
+                lambda: att(p.q1, p.kv1, p.a1),
+                lambda: ops.ikbo_linear(p.s, p.wkv2, out=p.kv2),
+                lambda: ops.ikbo_linear(p.a1.view(n, p.h * p.d), p.wq2, x_cand_add=p.e_c,
+                                        out=p.q2),
+                lambda: att(p.q2, p.kv2, p.a2)]
+    if cid == 4:
+        return [lambda: ops.glm_interaction(p.x_req, p.x_cand, p.cand_offsets, y_req=p.y_req,
+                                            y_cand=p.y_cand),
+                lambda: ops.ikbo_linear(p.y_cand, p.w_cand, x_req=p.y_req, w_req=p.w_req,
+                                        cand_offsets=p.cand_offsets, activation="relu",
+                                        out=p.out, workspace=p.ws)]
+    if cid == 5:
+        def att():
+            k, v = kvv(p.kv, p.h, p.d)
+            return ops.dca_attention(p.h1.view(n, 1, p.h, p.d), k, v, p.cand_offsets,
+                                     p.kv_offsets, out=p.attention)
+        return [lambda: ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
+                                        cand_offsets=p.cand_offsets, activation="relu",
+                                        out=p.h1, workspace=p.ws),
+                lambda: ops.ikbo_linear(p.h1, p.w2, out=p.out2),
+                lambda: ops.ikbo_linear(p.s, p.wkv, out=p.kv),
+                att]
+    raise ValueError(cid)
+
+
+def cpu_baseline(w, cid):
+    """The oracle, as it stands, on a bounded sample of the workload."""
+    import numpy as np
+    from oracle import pipelines as op
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
+    except Exception:   # noqa: BLE001 - reporting only
+        threads = 1
+    cores = min(threads, len(os.sched_getaffinity(0)))
+    if cid == 5:
+        n_s = 1024
+        rows = np.arange(n_s)
+        t0 = time.perf_counter()
+        op._request_kv(w.s, w.wk, w.wv, w.kv_offsets, [0])
+        t_kv = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        op.production_retrieval(w, rows=rows)
+        t_s = time.perf_counter() - t0
+        t_cand = max(t_s - t_kv, 1e-9) / n_s
+        total = w.n_req * t_kv + w.n_cand * t_cand
+        sample = (f"request 0: its K/V projection ({t_kv:.2f} s) plus the first {n_s} candidates "
+                  f"(IKBO linear, linear, DCA; {t_s - t_kv:.2f} s), float64 broadcast-then-"
+                  f"compute; extrapolated to {w.n_req} requests x {w.n_cand // w.n_req} "
+                  "candidates")
+    else:
+        n_s = min(w.n_cand, 4096)
+        rows = np.arange(n_s)
+        fn = op.PIPELINES[cid]
+        t0 = time.perf_counter()
+        fn(w, rows=rows)
+        t_s = time.perf_counter() - t0
+        total = t_s * w.n_cand / n_s
+        sample = f"first {n_s} candidates, extrapolated linearly to {w.n_cand}"
+    return {"value": w.n_cand / total, "unit": "candidates/s", "cores": int(cores),
+            "kind": "oracle", "sample": sample}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path "
+              f"(--gpus {args.gpus} requested). Requests shard independently across GPUs; "
+              "see the design notes.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_27744_amd import ops, pipelines, workloads as wl
+
+    ops.load_library()
+    log(f"generating workload {args.workload}")
+    w = wl.make_workload(args.workload)
+    log("uploading")
+    p = pipelines.prepare(w)
+    fns = timed_step_fns(p)
+    plan = op_plan(w)
+    assert len(plan) == len(fns)
+
+    stream = torch.cuda.current_stream()
+    log(f"warmup x{args.warmup}")
+    for _ in range(args.warmup):
+        pipelines.step(p)
+    torch.cuda.synchronize()
+
+    log(f"timing x{args.steps}")
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in fns] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        for i, fn in enumerate(fns):
+            ev[s][i][0].record(stream)
+            fn()
+            ev[s][i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = 1e3 * wall / args.steps
+    op_ms = [float(np.mean([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)]))
+             for i in range(len(fns))]
+
+    kernels = {}
+    fp32 = w.dtype == "f32"
+    for (name, flops, byts, bound), ms in zip(plan, op_ms):
+        tflops = flops / (ms * 1e-3) / 1e12
+        gbs = byts / (ms * 1e-3) / 1e9
+        peak = PEAK_FP32_TFLOPS if fp32 else PEAK_BF16_TFLOPS
+        kernels[name] = {"ms": round(ms, 4), "tflops": round(tflops, 2), "gbs": round(gbs, 1),
+                         "mfma_frac": round(tflops / peak, 4),
+                         "hbm_frac": round(gbs / PEAK_HBM_GBS, 4), "bound": bound}
+    dom = int(np.argmax(op_ms))
+    name, flops, byts, bound = plan[dom]
+    if bound == "hbm":
+        achieved, peak, unit = byts / (op_ms[dom] * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+    elif bound == "alu":
+        achieved, peak, unit = flops / (op_ms[dom] * 1e-3) / 1e12, PEAK_FP32_TFLOPS, "TFLOP/s"
+    else:
+        achieved, peak, unit = flops / (op_ms[dom] * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+    roofline = {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(w, args.workload)
+
+    names = {1: "tiny ROCS block", 2: "retrieval IKBO MLP", 3: "ranking two-layer DCA",
+             4: "GLM FM + IKBO linear", 5: "production-scale retrieval"}
+    line = {
+        "metric": "candidates/sec scored (IKBO linear + DCA) at 1 GPU; % of bf16 MFMA / HBM peak",
+        "value": round(w.n_cand / (ms_step * 1e-3), 1),
+        "unit": "candidates/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if fp32 else "bf16", "data": "synthetic",
+        "config": {"workload": f"{names[args.workload]}: {wl.WORKLOAD_NAMES[args.workload]}",
+                   "requests": w.n_req, "candidates": w.n_cand, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,202 @@
+/*
+ * rocs.h - C ABI of librocs, the MI355X (gfx950) IKBO inference hot path of
+ * ROCS (Request-Oriented Compute Sharing, arXiv 2607.27744).
+ *
+ * In-Kernel Broadcast Optimization (IKBO, Section 4) keeps request-side and
+ * candidate-side tensors at their natural batch sizes, R requests (B_r) and
+ * N candidates (B_c), and resolves the candidate -> request map m inside the
+ * consuming kernels instead of materialising a request-to-candidate
+ * broadcast. Here m is given as CSR offsets:
+ *
+ *   cand_offsets[R + 1], int32, device memory:
+ *     candidate n belongs to request r  iff  cand_offsets[r] <= n < cand_offsets[r+1]
+ *   so the candidates of one request are contiguous (Section 4.2.1 and 4.3.1
+ *   both rely on this ordering for cache locality).
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers to contiguous row-major arrays owned
+ *     by the caller. The library never allocates, frees or keeps them; it
+ *     holds no pointer after a call returns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     Work is enqueued asynchronously; nothing is synchronised. A fault in a
+ *     kernel surfaces at the caller's next synchronisation.
+ *   - Offsets arrays are trusted device data: offsets[0] == 0, non-decreasing,
+ *     offsets[R] equal to the row count they index. They are not read on the
+ *     host (that would need a synchronisation); malformed offsets give
+ *     undefined results. rocs_validate_offsets() checks them when wanted.
+ *   - Element types: ROCS_DTYPE_BF16 (bfloat16 storage, fp32 accumulation,
+ *     results rounded to nearest-even) or ROCS_DTYPE_F32 (fp32 throughout).
+ *     Inputs and outputs of one call share the dtype; bias and the linear
+ *     workspace are always fp32.
+ *   - Every call returns a rocs_status. On failure nothing has been enqueued,
+ *     and rocs_last_error_message() (thread-local) explains the failure.
+ *     R == 0 or N == 0 is a valid no-op (outputs that have no rows are not
+ *     touched; request-side outputs are still produced where they exist).
+ *   - Calls are reentrant; concurrent calls on different streams need
+ *     separate workspaces.
+ */
+#ifndef ROCS_H
+#define ROCS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ROCS_ABI_VERSION 1
+
+typedef enum rocs_status {
+  ROCS_OK = 0,
+  ROCS_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad size, bad enum, misalignment */
+  ROCS_ERR_UNSUPPORTED = 2,        /* valid request this build cannot run */
+  ROCS_ERR_WORKSPACE_TOO_SMALL = 3,
+  ROCS_ERR_HIP = 4                 /* the HIP runtime refused a launch */
+} rocs_status;
+
+typedef enum rocs_dtype { ROCS_DTYPE_F32 = 0, ROCS_DTYPE_BF16 = 1 } rocs_dtype;
+
+typedef enum rocs_activation { ROCS_ACT_NONE = 0, ROCS_ACT_RELU = 1 } rocs_activation;
+
+int32_t rocs_abi_version(void);
+const char* rocs_status_string(int32_t status);
+/* Detail of the calling thread's last non-OK status ("" if none). */
+const char* rocs_last_error_message(void);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_ikbo_linear: the candidate-side output of a two-group GLM linear
+ * (Eq. glm-linear with K = 2; Section 4.1 decomposition; Eq. broadcast_add;
+ * fusion of the broadcast-add into the GEMM epilogue, Section 4.2.1).
+ *
+ *   out[n][d] = act( sum_k w_cand[d][k] * xc[n][k]
+ *                  + sum_k w_req[d][k]  * x_req[m_n][k]   (= Z[m_n][d])
+ *                  + bias[d] )
+ *
+ * where xc = x_cand, or, when x_cand_add is not NULL, the GLM pointwise
+ * residual xc = round(x_cand + x_cand_add) computed elementwise in fp32 and
+ * rounded to the input dtype (Eq. glm-elementwise) before the product.
+ *
+ * The request-side product Z = x_req . w_req^T ([R, d_out], fp32) is computed
+ * once per request into the workspace, together with the expanded index map
+ * m ([N] int32); the candidate GEMM adds Z[m_n] in its epilogue. No
+ * candidate-batched copy of x_req or Z is ever formed.
+ *
+ *   x_req       [R, k_req]        request-side input; may be NULL iff k_req == 0
+ *   k_req       >= 0; 0 makes this a plain linear (no request term)
+ *   x_cand      [N, k_cand]       candidate-side input
+ *   x_cand_add  [N, k_cand] or NULL
+ *   k_cand      >= 1
+ *   w_req       [d_out, k_req]    W_CR in the paper's [out, in] orientation
+ *   w_cand      [d_out, k_cand]   W_CC
+ *   bias        [d_out] fp32 or NULL (zero)
+ *   cand_offsets [R + 1]          may be NULL iff k_req == 0
+ *   out         [N, d_out]        must not overlap any input
+ *   workspace   device memory of at least rocs_ikbo_linear_workspace_size()
+ *               bytes, 256-byte aligned; may be NULL when that size is 0.
+ *               Contents on entry are ignored; on return they are scratch.
+ *
+ * Fast path: bf16, k_req and k_cand multiples of 8, d_out a multiple of 4 and
+ * every pointer 16-byte aligned. Other shapes take a slower general kernel
+ * (the zero-padding transform of Section 4.2.4 restores the fast path).
+ * ---------------------------------------------------------------------------
+ */
+size_t rocs_ikbo_linear_workspace_size(int64_t num_requests, int64_t num_cand,
+                                       int64_t d_out, int64_t k_req);
+
+int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req,
+                         const void* x_cand, const void* x_cand_add, int64_t k_cand,
+                         const void* w_req, const void* w_cand, const float* bias,
+                         const int32_t* cand_offsets,
+                         int64_t num_requests, int64_t num_cand, int64_t d_out,
+                         int32_t dtype, int32_t activation,
+                         void* out, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_dca_attention: candidate-side Deep Cross Attention
+ * A^C = Attn(Q^C, S W_K, S W_V) (Section 3.2, Eq. dca-attention) with the
+ * request-batched K/V consumed directly (Section 4.3.1): every candidate of
+ * request r attends over r's history, which is read once per tile of that
+ * request's candidates and shared by all of them; no per-candidate K/V copy.
+ *
+ * For candidate n with r = m_n, query token t and head h:
+ *   s_j      = scale * <q[n][t][h][:], k[j][h][:]>   for kv_offsets[r] <= j < kv_offsets[r+1]
+ *   out[n][t][h][:] = sum_j softmax(s)_j * v[j][h][:]   (no mask)
+ * An empty history (L_r == 0) gives zeros.
+ *
+ *   q            [N, q_len, H, head_dim]
+ *   k, v         history rows packed request after request; row j of k
+ *                starts at k + j * kv_row_stride elements and holds
+ *                [H, head_dim]; same for v. kv_row_stride == 0 means
+ *                H * head_dim (dense [L_total, H, head_dim]). A larger stride
+ *                lets k and v be column slices of one projection output.
+ *   cand_offsets [R + 1]; kv_offsets [R + 1] (L_total = kv_offsets[R])
+ *   q_len >= 1, num_heads >= 1, 1 <= head_dim <= 256
+ *   softmax_scale  > 0, or <= 0 for 1/sqrt(head_dim)
+ *   out          [N, q_len, H, head_dim], must not overlap any input
+ *
+ * Fast path (bf16 MFMA kernel): bf16, head_dim 64 or 128, H*head_dim and
+ * kv_row_stride multiples of 8, pointers 16-byte aligned. Other cases run a
+ * general kernel.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
+                           const int32_t* cand_offsets, const int32_t* kv_offsets,
+                           int64_t num_requests, int64_t num_cand,
+                           int32_t q_len, int32_t num_heads, int32_t head_dim,
+                           int64_t kv_row_stride, float softmax_scale, int32_t dtype,
+                           void* out, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_glm_interaction: the two-group GLM-masked factorization machine
+ * (Eq. glm-fm, two-group form Eq. glm-fm-two-groups).
+ *
+ *   y_req[r]  = X^R_r (X^R_r)^T                      once per request,
+ *               [F_r, F_r] flattened row-major        -> [R, F_r * F_r]
+ *   y_cand[n] = [ X^C_n (X^R_{m_n})^T | X^C_n (X^C_n)^T ]  per candidate,
+ *               [F_c, F_r + F_c] flattened row-major  -> [N, F_c * (F_r + F_c)]
+ * The masked request-row/candidate-column block is structurally zero and is
+ * not produced.
+ *
+ *   x_req  [R, f_req, emb_dim]     x_cand [N, f_cand, emb_dim]
+ *   y_req  output or NULL (skip);  y_cand output or NULL (skip)
+ *
+ * Fast path (bf16 MFMA kernel): bf16, f_req a multiple of 16, f_cand in
+ * {2, 4, 8, 16}, emb_dim a multiple of 32, pointers 16-byte aligned. Other
+ * cases run a general kernel.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_glm_interaction(const void* x_req, const void* x_cand,
+                             const int32_t* cand_offsets,
+                             int64_t num_requests, int64_t num_cand,
+                             int32_t f_req, int32_t f_cand, int32_t emb_dim,
+                             int32_t dtype, void* y_req, void* y_cand, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * Index-map helpers (Section 4.1, m in {0..B_r-1}^{B_c}).
+ *
+ * rocs_request_ids: out_ids[n] = m_n for n < N, computed on the device by the
+ * same routine the linear kernel uses (exposed so index handling can be
+ * checked bit-exactly). out_ids is [N] int32.
+ *
+ * rocs_validate_offsets: copies offsets [count] to the host (synchronising
+ * `stream`) and checks offsets[0] == 0, non-decreasing, offsets[count-1] ==
+ * total. Returns ROCS_OK or ROCS_ERR_INVALID_ARGUMENT.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_request_ids(const int32_t* cand_offsets, int64_t num_requests,
+                         int64_t num_cand, int32_t* out_ids, void* stream);
+
+int32_t rocs_validate_offsets(const int32_t* offsets, int64_t count, int64_t total,
+                              void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ROCS_H */

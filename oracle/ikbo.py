@@ -87,7 +87,7 @@ def ikbo_linear(x_req, x_cand, w_req, w_cand, bias, cand_offsets, act="none",
     rows: optional candidate indices; only those outputs are computed.
     Returns float64 [N, D] (or [len(rows), D]).
     """
-    x_cand = _f64(x_cand)
+    x_cand = np.asarray(x_cand)          # converted chunk by chunk below
     w_cand = _f64(w_cand)
     n_cand = x_cand.shape[0]
     d_out = w_cand.shape[0]
@@ -106,9 +106,9 @@ def ikbo_linear(x_req, x_cand, w_req, w_cand, bias, cand_offsets, act="none",
     for s in range(0, sel.size, chunk):
         idx = sel[s:s + chunk]
         if k_req:
-            x_full = np.concatenate([x_req[m[idx]], x_cand[idx]], axis=1)
+            x_full = np.concatenate([x_req[m[idx]], _f64(x_cand[idx])], axis=1)
         else:
-            x_full = x_cand[idx]
+            x_full = _f64(x_cand[idx])
         out[s:s + chunk] = activation(x_full @ w_full.T + b, act)
     return out
 
@@ -245,7 +245,7 @@ def glm_fm_masked_blocks(x_req, x_cand, cand_offsets, rows=None):
     [N, F_r + F_c, F_r + F_c].
     """
     x_req = _f64(x_req)
-    x_cand = _f64(x_cand)
+    x_cand = np.asarray(x_cand)          # converted chunk by chunk below
     n_cand, f_c, _ = x_cand.shape
     f_r = x_req.shape[1]
     m = request_ids(check_offsets(cand_offsets, n_cand))
@@ -255,7 +255,7 @@ def glm_fm_masked_blocks(x_req, x_cand, cand_offsets, rows=None):
     out = np.empty((sel.size, f_r + f_c, f_r + f_c))
     for s in range(0, sel.size, _CHUNK // 4):
         idx = sel[s:s + _CHUNK // 4]
-        x_full = np.concatenate([x_req[m[idx]], x_cand[idx]], axis=1)
+        x_full = np.concatenate([x_req[m[idx]], _f64(x_cand[idx])], axis=1)
         out[s:s + idx.size] = (x_full @ np.transpose(x_full, (0, 2, 1))) * mask
     return out
 

@@ -1,0 +1,273 @@
+// C ABI of librocs: argument validation, fast-path selection, error reporting.
+// Nothing here touches tensor data; every operation runs in the kernels.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/rocs.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+int32_t fail(rocs_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return s;
+}
+
+int32_t ok() {
+  g_error.clear();
+  return ROCS_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+// Byte ranges [a, a + an) and [b, b + bn) intersect.
+bool overlap(const void* a, size_t an, const void* b, size_t bn) {
+  if (a == nullptr || b == nullptr || an == 0 || bn == 0) return false;
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + bn && y < x + an;
+}
+
+size_t align256(size_t n) { return (n + 255) & ~size_t(255); }
+
+bool valid_dtype(int32_t d) { return d == ROCS_DTYPE_F32 || d == ROCS_DTYPE_BF16; }
+size_t esize(int32_t d) { return d == ROCS_DTYPE_BF16 ? 2 : 4; }
+
+constexpr int64_t kMaxI32 = 2147483647;
+
+}  // namespace
+
+extern "C" {
+
+int32_t rocs_abi_version(void) { return ROCS_ABI_VERSION; }
+
+const char* rocs_status_string(int32_t s) {
+  switch (s) {
+    case ROCS_OK: return "ok";
+    case ROCS_ERR_INVALID_ARGUMENT: return "invalid argument";
+    case ROCS_ERR_UNSUPPORTED: return "unsupported";
+    case ROCS_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case ROCS_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* rocs_last_error_message(void) { return g_error.c_str(); }
+
+size_t rocs_ikbo_linear_workspace_size(int64_t num_requests, int64_t num_cand, int64_t d_out,
+                                       int64_t k_req) {
+  if (k_req <= 0 || num_requests <= 0 || num_cand <= 0 || d_out <= 0) return 0;
+  return align256((size_t)num_requests * (size_t)d_out * sizeof(float)) +
+         align256((size_t)num_cand * sizeof(int32_t));
+}
+
+int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
+                         const void* x_cand_add, int64_t k_cand, const void* w_req,
+                         const void* w_cand, const float* bias, const int32_t* cand_offsets,
+                         int64_t R, int64_t N, int64_t d_out, int32_t dtype, int32_t activation,
+                         void* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (activation != ROCS_ACT_NONE && activation != ROCS_ACT_RELU)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown activation %d", activation);
+  if (R < 0 || N < 0 || k_req < 0 || k_cand < 1 || d_out < 1)
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "sizes must satisfy R >= 0, N >= 0, k_req >= 0, k_cand >= 1, d_out >= 1 "
+                "(got R=%lld N=%lld k_req=%lld k_cand=%lld d_out=%lld)",
+                (long long)R, (long long)N, (long long)k_req, (long long)k_cand,
+                (long long)d_out);
+  if (N > kMaxI32 || R > kMaxI32 || k_req > kMaxI32 || k_cand > kMaxI32 || d_out > kMaxI32)
+    return fail(ROCS_ERR_UNSUPPORTED, "a size exceeds 2^31 - 1");
+  if (N == 0) return ok();
+  if (k_req > 0 && R == 0)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests to own them");
+  if (x_cand == nullptr || w_cand == nullptr || out == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "x_cand, w_cand and out must not be NULL");
+  if (k_req > 0 && (x_req == nullptr || w_req == nullptr || cand_offsets == nullptr))
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "k_req > 0 needs x_req, w_req and cand_offsets");
+  const size_t need = rocs_ikbo_linear_workspace_size(R, N, d_out, k_req);
+  if (need > 0) {
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(ROCS_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need,
+                  workspace == nullptr ? (size_t)0 : workspace_bytes);
+    if (!aligned(workspace, 256))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  }
+  const size_t es = esize(dtype);
+  const size_t out_bytes = (size_t)N * d_out * es;
+  const struct { const void* p; size_t n; const char* name; } ins[] = {
+      {x_req, (size_t)R * k_req * es, "x_req"},
+      {x_cand, (size_t)N * k_cand * es, "x_cand"},
+      {x_cand_add, (size_t)N * k_cand * es, "x_cand_add"},
+      {w_req, (size_t)d_out * k_req * es, "w_req"},
+      {w_cand, (size_t)d_out * k_cand * es, "w_cand"},
+      {bias, (size_t)d_out * sizeof(float), "bias"},
+      {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"},
+      {need > 0 ? workspace : nullptr, need, "workspace"},
+  };
+  for (const auto& in : ins)
+    if (overlap(out, out_bytes, in.p, in.n))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "out overlaps %s", in.name);
+  if (need > 0) {
+    const size_t zb = align256((size_t)R * d_out * sizeof(float));
+    const struct { const void* p; size_t n; const char* name; } inw[] = {
+        {x_req, (size_t)R * k_req * es, "x_req"}, {x_cand, (size_t)N * k_cand * es, "x_cand"},
+        {w_req, (size_t)d_out * k_req * es, "w_req"}, {w_cand, (size_t)d_out * k_cand * es, "w_cand"},
+        {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"}};
+    for (const auto& in : inw)
+      if (overlap(workspace, need, in.p, in.n))
+        return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace overlaps %s", in.name);
+    (void)zb;
+  }
+
+  rocs::LinearArgs a{};
+  a.x_req = x_req; a.x_cand = x_cand; a.x_cand_add = x_cand_add;
+  a.w_req = w_req; a.w_cand = w_cand; a.bias = bias; a.cand_offsets = cand_offsets;
+  a.R = R; a.N = N; a.k_req = k_req; a.k_cand = k_cand; a.d_out = d_out;
+  a.bf16 = dtype == ROCS_DTYPE_BF16;
+  a.relu = activation == ROCS_ACT_RELU;
+  a.out = out;
+  if (need > 0) {
+    a.z = static_cast<float*>(workspace);
+    a.ids = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) +
+                                       align256((size_t)R * d_out * sizeof(float)));
+  }
+  const bool fast = a.bf16 && k_cand % 8 == 0 && k_req % 8 == 0 && d_out % 4 == 0 &&
+                    aligned(x_cand, 16) && aligned(x_cand_add, 16) && aligned(w_cand, 16) &&
+                    aligned(x_req, 16) && aligned(w_req, 16) && aligned(bias, 16) &&
+                    aligned(out, 16);
+  const hipError_t e = rocs::launch_linear(a, fast, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_ikbo_linear: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
+                           const int32_t* cand_offsets, const int32_t* kv_offsets, int64_t R,
+                           int64_t N, int32_t q_len, int32_t num_heads, int32_t head_dim,
+                           int64_t kv_row_stride, float softmax_scale, int32_t dtype, void* out,
+                           void* stream) {
+  if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (R < 0 || N < 0 || q_len < 1 || num_heads < 1 || head_dim < 1 || kv_row_stride < 0)
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "need R >= 0, N >= 0, q_len >= 1, num_heads >= 1, head_dim >= 1, "
+                "kv_row_stride >= 0");
+  if (head_dim > 256) return fail(ROCS_ERR_UNSUPPORTED, "head_dim %d > 256", head_dim);
+  const int64_t row_elems = (int64_t)num_heads * head_dim;
+  const int64_t stride = kv_row_stride == 0 ? row_elems : kv_row_stride;
+  if (stride < row_elems)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "kv_row_stride %lld < num_heads * head_dim",
+                (long long)kv_row_stride);
+  if (N * q_len > kMaxI32 || R > kMaxI32 || (int64_t)num_heads > 65535)
+    return fail(ROCS_ERR_UNSUPPORTED, "batch too large");
+  if (N == 0) return ok();
+  if (R == 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests");
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || cand_offsets == nullptr ||
+      kv_offsets == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
+  const size_t es = esize(dtype);
+  const size_t out_bytes = (size_t)N * q_len * row_elems * es;
+  if (overlap(out, out_bytes, q, out_bytes) || overlap(out, out_bytes, k, 1) ||
+      overlap(out, out_bytes, v, 1) ||
+      overlap(out, out_bytes, cand_offsets, (size_t)(R + 1) * 4) ||
+      overlap(out, out_bytes, kv_offsets, (size_t)(R + 1) * 4))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "out overlaps an input");
+
+  rocs::AttentionArgs a{};
+  a.q = q; a.k = k; a.v = v; a.cand_offsets = cand_offsets; a.kv_offsets = kv_offsets;
+  a.R = R; a.N = N; a.q_len = q_len; a.heads = num_heads; a.head_dim = head_dim;
+  a.kv_stride = stride;
+  a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)head_dim);
+  a.bf16 = dtype == ROCS_DTYPE_BF16;
+  a.out = out;
+  const bool fast = a.bf16 && (head_dim == 64 || head_dim == 128) && stride % 8 == 0 &&
+                    aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16);
+  const hipError_t e = rocs::launch_attention(a, fast, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_dca_attention: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int32_t rocs_glm_interaction(const void* x_req, const void* x_cand, const int32_t* cand_offsets,
+                             int64_t R, int64_t N, int32_t f_req, int32_t f_cand, int32_t emb,
+                             int32_t dtype, void* y_req, void* y_cand, void* stream) {
+  if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (R < 0 || N < 0 || f_req < 1 || f_cand < 1 || emb < 1)
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "need R >= 0, N >= 0, f_req >= 1, f_cand >= 1, emb_dim >= 1");
+  if (R > kMaxI32 || N * f_cand > kMaxI32)
+    return fail(ROCS_ERR_UNSUPPORTED, "batch too large");
+  if (N > 0 && R == 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests");
+  if (y_cand == nullptr) N = 0;
+  if (R == 0 || (N == 0 && y_req == nullptr)) return ok();
+  if (x_req == nullptr || (N > 0 && (x_cand == nullptr || cand_offsets == nullptr)))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
+  if (cand_offsets == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "cand_offsets must not be NULL");
+  const size_t es = esize(dtype);
+  const size_t yr_bytes = (size_t)R * f_req * f_req * es;
+  const size_t yc_bytes = (size_t)N * f_cand * (f_req + f_cand) * es;
+  const size_t xr_bytes = (size_t)R * f_req * emb * es, xc_bytes = (size_t)N * f_cand * emb * es;
+  if (overlap(y_req, yr_bytes, x_req, xr_bytes) || overlap(y_req, yr_bytes, x_cand, xc_bytes) ||
+      overlap(y_cand, yc_bytes, x_req, xr_bytes) || overlap(y_cand, yc_bytes, x_cand, xc_bytes) ||
+      overlap(y_req, yr_bytes, y_cand, yc_bytes))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "outputs overlap inputs or each other");
+
+  rocs::InteractionArgs a{};
+  a.x_req = x_req; a.x_cand = x_cand; a.cand_offsets = cand_offsets;
+  a.R = R; a.N = N; a.f_req = f_req; a.f_cand = f_cand; a.emb = emb;
+  a.bf16 = dtype == ROCS_DTYPE_BF16;
+  a.y_req = y_req; a.y_cand = N > 0 ? y_cand : nullptr;
+  const bool fast = a.bf16 && f_req % 16 == 0 && (f_cand == 4 || f_cand == 8 || f_cand == 16) &&
+                    emb % 32 == 0 && aligned(x_req, 16) && aligned(x_cand, 16) &&
+                    aligned(y_req, 16) && aligned(y_cand, 16);
+  const hipError_t e = rocs::launch_interaction(a, fast, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess)
+    return fail(ROCS_ERR_HIP, "rocs_glm_interaction: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int32_t rocs_request_ids(const int32_t* cand_offsets, int64_t R, int64_t N, int32_t* out_ids,
+                         void* stream) {
+  if (R < 0 || N < 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "negative size");
+  if (N > kMaxI32 || R > kMaxI32) return fail(ROCS_ERR_UNSUPPORTED, "batch too large");
+  if (N == 0) return ok();
+  if (R == 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests");
+  if (cand_offsets == nullptr || out_ids == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
+  const hipError_t e = rocs::launch_request_ids(cand_offsets, R, N, out_ids,
+                                                static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_request_ids: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int32_t rocs_validate_offsets(const int32_t* offsets, int64_t count, int64_t total,
+                              void* stream) {
+  if (offsets == nullptr || count < 1)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "need a non-NULL offsets array of count >= 1");
+  std::vector<int32_t> h((size_t)count);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(h.data(), offsets, (size_t)count * sizeof(int32_t),
+                                hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_validate_offsets: %s", hipGetErrorString(e));
+  if (h[0] != 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "offsets[0] = %d, expected 0", h[0]);
+  for (int64_t i = 1; i < count; ++i)
+    if (h[(size_t)i] < h[(size_t)i - 1])
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "offsets decrease at index %lld", (long long)i);
+  if (h[(size_t)count - 1] != total)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "offsets end at %d, expected %lld",
+                h[(size_t)count - 1], (long long)total);
+  return ok();
+}
+
+}  // extern "C"

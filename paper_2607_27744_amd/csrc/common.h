@@ -1,0 +1,117 @@
+// Device-side helpers shared by the librocs kernels (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rocs {
+
+typedef __bf16 bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+constexpr int kNumXcd = 8;   // MI355X: 8 accelerator complex dies, 32 CUs each
+
+// D[16x16] += A[16x32] * B[32x16] on the matrix cores, bf16 in, fp32 out.
+// Lane l holds A[l % 16][8 (l / 16) .. +7], B[8 (l / 16) .. +7][l % 16] and
+// D[4 (l / 16) + i][l % 16] for i = 0..3.
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ u32x4 as_u32x4(bf16x8 v) { return __builtin_bit_cast(u32x4, v); }
+
+// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  bf16x2 r = {(bf16_t)a, (bf16_t)b};
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t p) { return __builtin_bit_cast(float, p << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t p) { return __builtin_bit_cast(float, p & 0xffff0000u); }
+
+template <typename T> __device__ __forceinline__ float load_f32(const T* p);
+template <> __device__ __forceinline__ float load_f32<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ float load_f32<bf16_t>(const bf16_t* p) { return (float)*p; }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float x) { return (bf16_t)x; }
+
+// 16-byte global load that returns zeros when `ok` is false.
+__device__ __forceinline__ u32x4 load16(const void* p, bool ok) {
+  u32x4 v = {0u, 0u, 0u, 0u};
+  if (ok) v = *reinterpret_cast<const u32x4*>(p);
+  return v;
+}
+
+// Owner of candidate n under CSR offsets: the largest r in [0, R) with
+// off[r] <= n. Empty requests (off[r] == off[r+1]) are skipped naturally.
+__device__ __forceinline__ int owner_of(const int32_t* __restrict__ off, int R, int64_t n) {
+  int lo = 0, hi = R - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if ((int64_t)off[mid] <= n) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Request tiling without a host-side pass over the offsets. Request r with
+// c_r = off[r] candidate rows before it owns tile slots
+//   g(r) = r + floor(c_r * rows_per_cand / TILE) ... g(r+1) - 1,
+// at least max(1, ceil(n_r * rows_per_cand / TILE)) of them, and the slots of
+// all requests are disjoint and below R + ceil(N * rows_per_cand / TILE). A
+// workgroup given slot t finds its request by binary search and its tile
+// index j = t - g(r); slots past the request's last tile exit at once.
+__device__ __forceinline__ int64_t tile_base(const int32_t* __restrict__ off, int r,
+                                             int rows_per_cand, int tile) {
+  return (int64_t)r + ((int64_t)off[r] * rows_per_cand) / tile;
+}
+
+__device__ __forceinline__ int request_of_slot(const int32_t* __restrict__ off, int R,
+                                               int64_t slot, int rows_per_cand, int tile) {
+  int lo = 0, hi = R - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (tile_base(off, mid, rows_per_cand, tile) <= slot) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Workgroups are dispatched round-robin over the XCDs (workgroup b runs on
+// XCD b % 8), and each XCD has its own L2. Renumber them so that consecutive
+// logical indices run on the same XCD: work items that share operands
+// (one candidate tile across output tiles, one request's K/V across candidate
+// tiles) then hit the same L2. A bijection on [0, G).
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t G) {
+  const uint32_t x = b % kNumXcd, i = b / kNumXcd;
+  const uint32_t q = G / kNumXcd, rem = G % kNumXcd;
+  return x * q + (x < rem ? x : rem) + i;
+}
+
+// Max over lanes l, l^16, l^32, l^48 (the four 16-lane rows of the wave).
+__device__ __forceinline__ float max_across_rows(float v) {
+  const int iv = __builtin_bit_cast(int, v);
+  auto s16 = __builtin_amdgcn_permlane16_swap(iv, iv, false, false);
+  v = fmaxf(__builtin_bit_cast(float, (int)s16[0]), __builtin_bit_cast(float, (int)s16[1]));
+  const int jv = __builtin_bit_cast(int, v);
+  auto s32 = __builtin_amdgcn_permlane32_swap(jv, jv, false, false);
+  return fmaxf(__builtin_bit_cast(float, (int)s32[0]), __builtin_bit_cast(float, (int)s32[1]));
+}
+
+__device__ __forceinline__ float sum_across_rows(float v) {
+  const int iv = __builtin_bit_cast(int, v);
+  auto s16 = __builtin_amdgcn_permlane16_swap(iv, iv, false, false);
+  v = __builtin_bit_cast(float, (int)s16[0]) + __builtin_bit_cast(float, (int)s16[1]);
+  const int jv = __builtin_bit_cast(int, v);
+  auto s32 = __builtin_amdgcn_permlane32_swap(jv, jv, false, false);
+  return __builtin_bit_cast(float, (int)s32[0]) + __builtin_bit_cast(float, (int)s32[1]);
+}
+
+}  // namespace rocs

@@ -1,0 +1,56 @@
+// Internal launcher interface between the C ABI layer and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rocs {
+
+struct LinearArgs {
+  const void* x_req;
+  const void* x_cand;
+  const void* x_cand_add;
+  const void* w_req;
+  const void* w_cand;
+  const float* bias;
+  const int32_t* cand_offsets;
+  int64_t R, N, k_req, k_cand, d_out;
+  bool bf16, relu;
+  void* out;
+  float* z;          // [R, d_out] workspace (k_req > 0)
+  int32_t* ids;      // [N] workspace (k_req > 0)
+};
+
+struct AttentionArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* cand_offsets;
+  const int32_t* kv_offsets;
+  int64_t R, N;
+  int q_len, heads, head_dim;
+  int64_t kv_stride;   // elements between history rows
+  float scale;
+  bool bf16;
+  void* out;
+};
+
+struct InteractionArgs {
+  const void* x_req;
+  const void* x_cand;
+  const int32_t* cand_offsets;
+  int64_t R, N;
+  int f_req, f_cand, emb;
+  bool bf16;
+  void* y_req;
+  void* y_cand;
+};
+
+// Each returns hipSuccess or the launch error.
+hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t* ids,
+                              hipStream_t s);
+hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s);
+hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s);
+hipError_t launch_interaction(const InteractionArgs& a, bool fast, hipStream_t s);
+
+}  // namespace rocs

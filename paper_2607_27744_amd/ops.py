@@ -1,0 +1,193 @@
+"""Torch-facing binding of librocs: argument marshalling only.
+
+Each function checks shapes, dtypes and devices, allocates outputs (and the
+linear's workspace) with torch when the caller does not pass them, and calls
+the C entry point of the same name on the current HIP stream. Every step of
+the computation runs in the library's kernels; there is no Python or CPU
+fallback, and a missing library raises.
+"""
+
+import ctypes
+
+import torch
+
+from . import _lib
+
+__all__ = [
+    "load_library", "ikbo_linear", "linear_workspace_size", "dca_attention",
+    "glm_interaction", "request_ids", "validate_offsets", "RocsError",
+]
+
+RocsError = _lib.RocsError
+_ACT = {"none": _lib.ACT_NONE, None: _lib.ACT_NONE, "relu": _lib.ACT_RELU}
+
+
+def load_library():
+    return _lib.load()
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return _lib.DTYPE_BF16
+    if t.dtype == torch.float32:
+        return _lib.DTYPE_F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bfloat16 or float32)")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(cond, msg):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _on_gpu(*ts):
+    dev = None
+    for t in ts:
+        if t is None:
+            continue
+        _need(t.is_cuda, "all tensors must be on the GPU")
+        dev = t.device if dev is None else dev
+        _need(t.device == dev, "all tensors must be on the same GPU")
+
+
+def _offsets(off, n_req):
+    _need(off.dtype == torch.int32 and off.dim() == 1 and off.is_contiguous(),
+          "offsets must be a contiguous 1-D int32 tensor")
+    _need(off.numel() == n_req + 1, f"offsets need {n_req + 1} entries, got {off.numel()}")
+
+
+def linear_workspace_size(num_requests, num_cand, d_out, k_req):
+    return int(_lib.load().rocs_ikbo_linear_workspace_size(num_requests, num_cand, d_out, k_req))
+
+
+def ikbo_linear(x_cand, w_cand, *, x_req=None, w_req=None, cand_offsets=None, bias=None,
+                activation="none", x_cand_add=None, out=None, workspace=None, stream=None):
+    """out[n] = act(w_cand @ xc[n] + w_req @ x_req[m_n] + bias), xc = x_cand (+ x_cand_add).
+
+    x_cand [N, K_c], w_cand [D, K_c], x_req [R, K_r], w_req [D, K_r] (paper's [out, in]
+    orientation), cand_offsets [R + 1] int32, bias [D] float32.
+    """
+    lib = _lib.load()
+    _need(x_cand.dim() == 2 and w_cand.dim() == 2, "x_cand and w_cand must be 2-D")
+    n_cand, k_cand = x_cand.shape
+    d_out = w_cand.shape[0]
+    _need(w_cand.shape[1] == k_cand, "w_cand must be [d_out, k_cand]")
+    code = _dtype_code(x_cand)
+    for t in (w_cand, x_req, w_req, x_cand_add):
+        _need(t is None or t.dtype == x_cand.dtype, "inputs must share one dtype")
+    if x_req is not None:
+        _need(w_req is not None and cand_offsets is not None,
+              "x_req needs w_req and cand_offsets")
+        _need(x_req.dim() == 2 and w_req.dim() == 2, "x_req and w_req must be 2-D")
+        n_req, k_req = x_req.shape
+        _need(w_req.shape == (d_out, k_req), "w_req must be [d_out, k_req]")
+    else:
+        k_req = 0
+        n_req = 0 if cand_offsets is None else cand_offsets.numel() - 1
+    if cand_offsets is not None:
+        _offsets(cand_offsets, n_req)
+    if x_cand_add is not None:
+        _need(x_cand_add.shape == x_cand.shape, "x_cand_add must match x_cand")
+    if bias is not None:
+        _need(bias.dtype == torch.float32 and bias.shape == (d_out,), "bias must be float32 [d_out]")
+    for t in (x_cand, w_cand, x_req, w_req, x_cand_add, bias):
+        _need(t is None or t.is_contiguous(), "tensors must be contiguous")
+    if out is None:
+        out = torch.empty((n_cand, d_out), dtype=x_cand.dtype, device=x_cand.device)
+    _need(out.shape == (n_cand, d_out) and out.dtype == x_cand.dtype and out.is_contiguous(),
+          "out must be a contiguous [N, d_out] tensor of the input dtype")
+    need = int(lib.rocs_ikbo_linear_workspace_size(n_req, n_cand, d_out, k_req))
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x_cand.device)
+    _on_gpu(x_cand, w_cand, x_req, w_req, cand_offsets, bias, x_cand_add, out, workspace)
+    _need(activation in _ACT, f"activation must be one of {sorted(k for k in _ACT if k)}")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _lib.check(lib.rocs_ikbo_linear(
+        _ptr(x_req), k_req, _ptr(x_cand), _ptr(x_cand_add), k_cand, _ptr(w_req), _ptr(w_cand),
+        _ptr(bias), _ptr(cand_offsets), n_req, n_cand, d_out, code, _ACT[activation],
+        _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)), "rocs_ikbo_linear")
+    return out
+
+
+def dca_attention(q, k, v, cand_offsets, kv_offsets, *, scale=None, out=None, stream=None):
+    """Candidate-side DCA: q [N, T, H, d]; k, v [L_total, H, d] (rows may be strided,
+    e.g. column slices of one [L, 2 H d] projection); offsets int32 [R + 1]."""
+    lib = _lib.load()
+    _need(q.dim() == 4 and q.is_contiguous(), "q must be a contiguous [N, T, H, d] tensor")
+    n_cand, q_len, heads, dim = q.shape
+    _need(k.dim() == 3 and v.dim() == 3 and k.shape == v.shape, "k and v must be [L, H, d]")
+    _need(k.shape[1:] == (heads, dim), "k/v heads and head_dim must match q")
+    _need(k.stride(2) == 1 and k.stride(1) == dim and v.stride(2) == 1 and v.stride(1) == dim,
+          "k/v rows must be dense [H, d] blocks")
+    _need(k.stride(0) == v.stride(0), "k and v must share a row stride")
+    for t in (k, v):
+        _need(t.dtype == q.dtype, "q, k, v must share one dtype")
+    n_req = cand_offsets.numel() - 1
+    _offsets(cand_offsets, n_req)
+    _offsets(kv_offsets, n_req)
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out.shape == q.shape and out.dtype == q.dtype and out.is_contiguous(),
+          "out must match q")
+    _on_gpu(q, k, v, cand_offsets, kv_offsets, out)
+    stride = k.stride(0) if k.shape[0] > 1 else heads * dim
+    _lib.check(lib.rocs_dca_attention(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(cand_offsets), _ptr(kv_offsets), n_req, n_cand,
+        q_len, heads, dim, stride, float(scale or 0.0), _dtype_code(q), _ptr(out),
+        _stream(stream)), "rocs_dca_attention")
+    return out
+
+
+def glm_interaction(x_req, x_cand, cand_offsets, *, request_side=True, candidate_side=True,
+                    y_req=None, y_cand=None, stream=None):
+    """GLM FM: returns (y_req [R, F_r^2] or None, y_cand [N, F_c (F_r + F_c)] or None)."""
+    lib = _lib.load()
+    _need(x_req.dim() == 3 and x_cand.dim() == 3, "x_req / x_cand must be [rows, fields, emb]")
+    n_req, f_req, emb = x_req.shape
+    n_cand, f_cand, emb_c = x_cand.shape
+    _need(emb == emb_c, "embedding widths differ")
+    _need(x_req.dtype == x_cand.dtype, "x_req and x_cand must share one dtype")
+    _need(x_req.is_contiguous() and x_cand.is_contiguous(), "inputs must be contiguous")
+    _offsets(cand_offsets, n_req)
+    if request_side and y_req is None:
+        y_req = torch.empty((n_req, f_req * f_req), dtype=x_req.dtype, device=x_req.device)
+    if candidate_side and y_cand is None:
+        y_cand = torch.empty((n_cand, f_cand * (f_req + f_cand)), dtype=x_req.dtype,
+                             device=x_req.device)
+    for t, shape in ((y_req, (n_req, f_req * f_req)),
+                     (y_cand, (n_cand, f_cand * (f_req + f_cand)))):
+        _need(t is None or (t.shape == shape and t.dtype == x_req.dtype and t.is_contiguous()),
+              "output shape / dtype mismatch")
+    _on_gpu(x_req, x_cand, cand_offsets, y_req, y_cand)
+    _lib.check(lib.rocs_glm_interaction(
+        _ptr(x_req), _ptr(x_cand), _ptr(cand_offsets), n_req, n_cand, f_req, f_cand, emb,
+        _dtype_code(x_req), _ptr(y_req if request_side else None),
+        _ptr(y_cand if candidate_side else None), _stream(stream)), "rocs_glm_interaction")
+    return (y_req if request_side else None), (y_cand if candidate_side else None)
+
+
+def request_ids(cand_offsets, num_cand, *, stream=None):
+    """m_n for every candidate, computed on the device (int32 [N])."""
+    lib = _lib.load()
+    n_req = cand_offsets.numel() - 1
+    _offsets(cand_offsets, n_req)
+    out = torch.empty(num_cand, dtype=torch.int32, device=cand_offsets.device)
+    _on_gpu(cand_offsets, out)
+    _lib.check(lib.rocs_request_ids(_ptr(cand_offsets), n_req, num_cand, _ptr(out),
+                                    _stream(stream)), "rocs_request_ids")
+    return out
+
+
+def validate_offsets(offsets, total, *, stream=None):
+    """Host-side check of device offsets (synchronises the stream)."""
+    lib = _lib.load()
+    _lib.check(lib.rocs_validate_offsets(_ptr(offsets), offsets.numel(), total,
+                                         _stream(stream)), "rocs_validate_offsets")

@@ -1,0 +1,154 @@
+"""The five benchmark pipelines on the GPU, as sequences of librocs calls.
+
+`prepare(w)` uploads a workload (built by `workloads.make_workload`) once:
+inputs to HBM, weights in the layout the kernels take (the paper's [out, in]
+orientation; K and V projection weights of one layer stacked so both come out
+of one GEMM), and every output and workspace buffer preallocated. `step(p)`
+then enqueues one pass of the hot path on the current stream and allocates
+nothing. Host work here is argument marshalling only.
+"""
+
+from types import SimpleNamespace
+
+import numpy as np
+import torch
+
+from . import ops
+
+
+def _bf16(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev, torch.bfloat16)
+
+
+def _f32(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+
+
+def _i32(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+
+def _ws(n_req, n_cand, d_out, k_req, dev):
+    size = ops.linear_workspace_size(n_req, n_cand, d_out, k_req)
+    return torch.empty(max(size, 1), dtype=torch.uint8, device=dev)
+
+
+def prepare(w, device="cuda"):
+    dev = torch.device(device)
+    p = SimpleNamespace(config_id=w.config_id, n_cand=w.n_cand, n_req=w.n_req, dev=dev)
+    p.cand_offsets = _i32(w.cand_offsets, dev)
+    cid = w.config_id
+    if cid == 1:
+        p.x_req, p.x_cand = _f32(w.x_req, dev), _f32(w.x_cand, dev)
+        p.w_req, p.w_cand = _f32(w.w_req, dev), _f32(w.w_cand, dev)
+        p.q, p.k, p.v = _f32(w.q, dev), _f32(w.k, dev), _f32(w.v, dev)
+        p.kv_offsets = _i32(w.kv_offsets, dev)
+        p.linear = torch.empty((w.n_cand, 256), dtype=torch.float32, device=dev)
+        p.attention = torch.empty_like(p.q)
+        p.ws = _ws(w.n_req, w.n_cand, 256, 256, dev)
+    elif cid == 2:
+        p.x_req, p.x_cand = _bf16(w.x_req, dev), _bf16(w.x_cand, dev)
+        p.w1_req, p.w1_cand, p.w2 = (_bf16(w.w1_req, dev), _bf16(w.w1_cand, dev),
+                                     _bf16(w.w2, dev))
+        p.h1 = torch.empty((w.n_cand, 512), dtype=torch.bfloat16, device=dev)
+        p.out = torch.empty((w.n_cand, 256), dtype=torch.bfloat16, device=dev)
+        p.ws = _ws(w.n_req, w.n_cand, 512, 1024, dev)
+    elif cid == 3:
+        h, d = w.n_heads, w.head_dim
+        p.kv_offsets = _i32(w.kv_offsets, dev)
+        p.e_c, p.s = _bf16(w.e_c, dev), _bf16(w.s, dev)
+        p.wq1, p.wq2 = _bf16(w.wq1, dev), _bf16(w.wq2, dev)
+        p.wkv1 = _bf16(np.concatenate([w.wk1, w.wv1], axis=0), dev)
+        p.wkv2 = _bf16(np.concatenate([w.wk2, w.wv2], axis=0), dev)
+        l_tot = w.s.shape[0]
+        p.kv1 = torch.empty((l_tot, 2 * h * d), dtype=torch.bfloat16, device=dev)
+        p.kv2 = torch.empty_like(p.kv1)
+        p.q1 = torch.empty((w.n_cand, h * d), dtype=torch.bfloat16, device=dev)
+        p.q2 = torch.empty_like(p.q1)
+        p.a1 = torch.empty((w.n_cand, 1, h, d), dtype=torch.bfloat16, device=dev)
+        p.a2 = torch.empty_like(p.a1)
+        p.h, p.d = h, d
+    elif cid == 4:
+        p.x_req, p.x_cand = _bf16(w.x_req, dev), _bf16(w.x_cand, dev)
+        p.w_req, p.w_cand = _bf16(w.w_req, dev), _bf16(w.w_cand, dev)
+        p.y_req = torch.empty((w.n_req, w.f_req * w.f_req), dtype=torch.bfloat16, device=dev)
+        p.y_cand = torch.empty((w.n_cand, w.f_cand * (w.f_req + w.f_cand)),
+                               dtype=torch.bfloat16, device=dev)
+        p.out = torch.empty((w.n_cand, 512), dtype=torch.bfloat16, device=dev)
+        p.ws = _ws(w.n_req, w.n_cand, 512, w.f_req * w.f_req, dev)
+    elif cid == 5:
+        h, d = w.n_heads, w.head_dim
+        p.kv_offsets = _i32(w.kv_offsets, dev)
+        p.x_req, p.x_cand = _bf16(w.x_req, dev), _bf16(w.x_cand, dev)
+        p.w1_req, p.w1_cand, p.w2 = (_bf16(w.w1_req, dev), _bf16(w.w1_cand, dev),
+                                     _bf16(w.w2, dev))
+        p.s = _bf16(w.s, dev)
+        p.wkv = _bf16(np.concatenate([w.wk, w.wv], axis=0), dev)
+        p.h1 = torch.empty((w.n_cand, h * d), dtype=torch.bfloat16, device=dev)
+        p.out2 = torch.empty((w.n_cand, 256), dtype=torch.bfloat16, device=dev)
+        p.kv = torch.empty((w.s.shape[0], 2 * h * d), dtype=torch.bfloat16, device=dev)
+        p.attention = torch.empty((w.n_cand, 1, h, d), dtype=torch.bfloat16, device=dev)
+        p.ws = _ws(w.n_req, w.n_cand, h * d, 2048, dev)
+        p.h, p.d = h, d
+    else:
+        raise ValueError(f"unknown workload {cid}")
+    return p
+
+
+def _kv_views(kv, h, d):
+    return kv[:, :h * d].view(-1, h, d), kv[:, h * d:].view(-1, h, d)
+
+
+def step(p):
+    """One pass of the workload's hot path (enqueue only)."""
+    cid = p.config_id
+    if cid == 1:
+        ops.ikbo_linear(p.x_cand, p.w_cand, x_req=p.x_req, w_req=p.w_req,
+                        cand_offsets=p.cand_offsets, activation="relu", out=p.linear,
+                        workspace=p.ws)
+        ops.dca_attention(p.q, p.k, p.v, p.cand_offsets, p.kv_offsets, out=p.attention)
+    elif cid == 2:
+        ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
+                        cand_offsets=p.cand_offsets, activation="relu", out=p.h1,
+                        workspace=p.ws)
+        ops.ikbo_linear(p.h1, p.w2, out=p.out)
+    elif cid == 3:
+        n = p.n_cand
+        ops.ikbo_linear(p.s, p.wkv1, out=p.kv1)
+        ops.ikbo_linear(p.e_c, p.wq1, out=p.q1)
+        k1, v1 = _kv_views(p.kv1, p.h, p.d)
+        ops.dca_attention(p.q1.view(n, 1, p.h, p.d), k1, v1, p.cand_offsets, p.kv_offsets,
+                          out=p.a1)
+        ops.ikbo_linear(p.s, p.wkv2, out=p.kv2)
+        ops.ikbo_linear(p.a1.view(n, p.h * p.d), p.wq2, x_cand_add=p.e_c, out=p.q2)
+        k2, v2 = _kv_views(p.kv2, p.h, p.d)
+        ops.dca_attention(p.q2.view(n, 1, p.h, p.d), k2, v2, p.cand_offsets, p.kv_offsets,
+                          out=p.a2)
+    elif cid == 4:
+        ops.glm_interaction(p.x_req, p.x_cand, p.cand_offsets, y_req=p.y_req, y_cand=p.y_cand)
+        ops.ikbo_linear(p.y_cand, p.w_cand, x_req=p.y_req, w_req=p.w_req,
+                        cand_offsets=p.cand_offsets, activation="relu", out=p.out,
+                        workspace=p.ws)
+    elif cid == 5:
+        n = p.n_cand
+        ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
+                        cand_offsets=p.cand_offsets, activation="relu", out=p.h1,
+                        workspace=p.ws)
+        ops.ikbo_linear(p.h1, p.w2, out=p.out2)
+        ops.ikbo_linear(p.s, p.wkv, out=p.kv)
+        k, v = _kv_views(p.kv, p.h, p.d)
+        ops.dca_attention(p.h1.view(n, 1, p.h, p.d), k, v, p.cand_offsets, p.kv_offsets,
+                          out=p.attention)
+    return p
+
+
+def outputs(p):
+    """Final outputs of the pipeline (name -> device tensor)."""
+    return {
+        1: lambda: {"linear": p.linear, "attention": p.attention},
+        2: lambda: {"h1": p.h1, "out": p.out},
+        3: lambda: {"q1": p.q1, "a1": p.a1.view(p.n_cand, -1), "q2": p.q2,
+                    "a2": p.a2.view(p.n_cand, -1)},
+        4: lambda: {"y_req": p.y_req, "y_cand": p.y_cand, "out": p.out},
+        5: lambda: {"h1": p.h1, "out2": p.out2, "attention": p.attention.view(p.n_cand, -1)},
+    }[p.config_id]()

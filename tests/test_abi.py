@@ -1,0 +1,124 @@
+"""C ABI checks that need no GPU: the library loads, exports exactly what
+include/rocs.h declares, and rejects bad arguments before any HIP call."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_27744_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rocs.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2607_27744_amd import build
+        build.build()
+    return _lib.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rocs_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported_and_bound(lib):
+    names = _declared()
+    assert len(names) == 9
+    assert sorted(_lib.SIGNATURES) == names
+    for n in names:
+        assert hasattr(lib, n)
+
+
+def test_version_and_status_strings(lib):
+    assert lib.rocs_abi_version() == _lib.ABI_VERSION
+    assert lib.rocs_status_string(0) == b"ok"
+    assert lib.rocs_status_string(3) == b"workspace too small"
+    assert lib.rocs_status_string(99) == b"unknown status"
+
+
+def test_workspace_size(lib):
+    assert lib.rocs_ikbo_linear_workspace_size(4, 256, 256, 0) == 0
+    assert lib.rocs_ikbo_linear_workspace_size(0, 256, 256, 8) == 0
+    # Z: 4*256 floats = 4096 bytes; ids: 256 int32 = 1024 bytes (256-aligned)
+    assert lib.rocs_ikbo_linear_workspace_size(4, 256, 256, 128) == 4096 + 1024
+    assert lib.rocs_ikbo_linear_workspace_size(3, 5, 7, 8) == 256 + 256
+
+
+P = ctypes.c_void_p
+FAKE = [P(0x10000 * (i + 1)) for i in range(12)]     # never dereferenced
+
+
+def _linear(lib, **kw):
+    args = dict(x_req=FAKE[0], k_req=8, x_cand=FAKE[1], x_add=None, k_cand=8, w_req=FAKE[2],
+                w_cand=FAKE[3], bias=None, off=FAKE[4], R=2, N=16, D=8, dtype=1, act=1,
+                out=FAKE[5], ws=FAKE[6], ws_bytes=1 << 20, stream=None)
+    args.update(kw)
+    return lib.rocs_ikbo_linear(*args.values())
+
+
+def test_linear_argument_errors(lib):
+    assert _linear(lib, dtype=7) == _lib.INVALID_ARGUMENT
+    assert b"dtype" in lib.rocs_last_error_message()
+    assert _linear(lib, act=5) == _lib.INVALID_ARGUMENT
+    assert _linear(lib, k_cand=0) == _lib.INVALID_ARGUMENT
+    assert _linear(lib, R=0) == _lib.INVALID_ARGUMENT
+    assert _linear(lib, x_cand=None) == _lib.INVALID_ARGUMENT
+    assert _linear(lib, off=None) == _lib.INVALID_ARGUMENT
+    assert _linear(lib, ws_bytes=16) == _lib.WORKSPACE_TOO_SMALL
+    assert _linear(lib, ws=None) == _lib.WORKSPACE_TOO_SMALL
+    assert _linear(lib, ws=P(0x60010)) == _lib.INVALID_ARGUMENT       # not 256-aligned
+    assert _linear(lib, out=P(0x20000 + 8)) == _lib.INVALID_ARGUMENT  # overlaps x_cand
+    assert b"overlaps" in lib.rocs_last_error_message()
+    assert _linear(lib, N=1 << 40) == _lib.UNSUPPORTED
+    # N == 0 is a no-op that never touches the device.
+    assert _linear(lib, N=0) == _lib.OK
+    assert lib.rocs_last_error_message() == b""
+
+
+def test_attention_argument_errors(lib):
+    def call(**kw):
+        a = dict(q=FAKE[0], k=FAKE[1], v=FAKE[2], co=FAKE[3], ko=FAKE[4], R=2, N=4, T=1, H=2,
+                 d=64, stride=0, scale=0.0, dtype=1, out=FAKE[5], stream=None)
+        a.update(kw)
+        return lib.rocs_dca_attention(*a.values())
+    assert call(dtype=3) == _lib.INVALID_ARGUMENT
+    assert call(T=0) == _lib.INVALID_ARGUMENT
+    assert call(d=300) == _lib.UNSUPPORTED
+    assert call(stride=64) == _lib.INVALID_ARGUMENT        # < H * d
+    assert call(k=None) == _lib.INVALID_ARGUMENT
+    assert call(R=0) == _lib.INVALID_ARGUMENT
+    assert call(out=FAKE[0]) == _lib.INVALID_ARGUMENT      # out aliases q
+    assert call(N=0) == _lib.OK
+
+
+def test_interaction_argument_errors(lib):
+    def call(**kw):
+        a = dict(xr=FAKE[0], xc=FAKE[1], co=FAKE[2], R=2, N=4, fr=16, fc=8, e=32, dtype=1,
+                 yr=FAKE[3], yc=FAKE[4], stream=None)
+        a.update(kw)
+        return lib.rocs_glm_interaction(*a.values())
+    assert call(dtype=2) == _lib.INVALID_ARGUMENT
+    assert call(fc=0) == _lib.INVALID_ARGUMENT
+    assert call(xr=None) == _lib.INVALID_ARGUMENT
+    assert call(co=None) == _lib.INVALID_ARGUMENT
+    assert call(yc=FAKE[0]) == _lib.INVALID_ARGUMENT       # output overlaps x_req
+    assert call(R=0, N=0) == _lib.OK
+
+
+def test_request_ids_and_validate_errors(lib):
+    assert lib.rocs_request_ids(FAKE[0], 0, 5, FAKE[1], None) == _lib.INVALID_ARGUMENT
+    assert lib.rocs_request_ids(None, 2, 5, FAKE[1], None) == _lib.INVALID_ARGUMENT
+    assert lib.rocs_request_ids(FAKE[0], 2, 0, FAKE[1], None) == _lib.OK
+    assert lib.rocs_validate_offsets(None, 3, 5, None) == _lib.INVALID_ARGUMENT
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(_lib, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        _lib.load(str(tmp_path / "librocs.so"))

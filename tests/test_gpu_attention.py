@@ -1,0 +1,100 @@
+"""GPU parity: rocs_dca_attention against the oracle (explicit K/V broadcast)."""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import assert_close, dev_bf16, dev_f32, dev_i32, host
+from oracle import ikbo
+from oracle.bf16 import round_bf16
+from paper_2607_27744_amd import ops
+from paper_2607_27744_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+# (candidate counts, history lengths): empty requests, empty histories,
+# histories of 1 and around the 64-key stage, candidate counts around the
+# 256-row tile.
+SHAPES = [
+    ([300, 1, 0, 211], [70, 5, 0, 129]),
+    ([256, 257, 255], [64, 65, 63]),
+    ([1], [1]),
+    ([40, 500], [1000, 300]),
+]
+
+
+def _attn(case, scale=None):
+    return host(ops.dca_attention(dev_bf16(case.q), dev_bf16(case.k), dev_bf16(case.v),
+                                  dev_i32(case.cand_offsets), dev_i32(case.kv_offsets),
+                                  scale=scale))
+
+
+def _want(case, scale=None):
+    return round_bf16(ikbo.dca_attention(case.q, case.k, case.v, case.cand_offsets,
+                                         case.kv_offsets, scale=scale, mode="explicit"))
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"n{sum(s[0])}-L{sum(s[1])}")
+@pytest.mark.parametrize("head_dim", [64, 128])
+@pytest.mark.parametrize("q_len", [1, 3])
+def test_attention_parity(gpu_lib, shape, head_dim, q_len):
+    counts, lens = shape
+    case = wl.attention_case(counts, lens, 2, head_dim, q_len=q_len, seed=head_dim + q_len)
+    assert_close(_attn(case), _want(case), f"dca {shape} d{head_dim} T{q_len}")
+
+
+def test_peaked_scores_exercise_rescaling(gpu_lib):
+    # Large logits: the running max moves by far more than the lazy threshold.
+    case = wl.attention_case([300, 90], [400, 257], 4, 64, seed=9, q_std=6.0)
+    assert_close(_attn(case), _want(case), "peaked")
+    assert_close(_attn(case, scale=0.01), _want(case, scale=0.01), "explicit scale")
+
+
+def test_single_key_is_exact(gpu_lib):
+    # L = 1: the one weight is exactly 1, so the output is that value row.
+    case = wl.attention_case([37, 300], [1, 1], 2, 128, seed=10, q_std=4.0)
+    got = _attn(case)
+    np.testing.assert_array_equal(got[:37, 0], np.broadcast_to(case.v[0], (37, 2, 128)))
+    np.testing.assert_array_equal(got[37:, 0], np.broadcast_to(case.v[1], (300, 2, 128)))
+
+
+def test_request_separation_probe(gpu_lib):
+    # V rows of request r all equal 4 r: a candidate routed to the wrong
+    # request would be off by at least 4.
+    counts, lens = np.array([50, 0, 300, 7]), np.array([100, 64, 3, 190])
+    case = wl.attention_case(counts, lens, 2, 64, seed=11)
+    case.v = np.repeat(4.0 * np.repeat(np.arange(4), lens), 2 * 64).reshape(-1, 2, 64).astype(np.float32)
+    got = _attn(case)
+    want = np.repeat(4.0 * np.arange(4), counts)
+    np.testing.assert_allclose(got, np.broadcast_to(want[:, None, None, None], got.shape), atol=0.02)
+
+
+def test_strided_kv_slices_of_one_projection(gpu_lib):
+    case = wl.attention_case([120, 130], [100, 140], 2, 64, seed=12)
+    kv = torch.cat([dev_bf16(case.k).reshape(-1, 128), dev_bf16(case.v).reshape(-1, 128)], dim=1)
+    k = kv[:, :128].view(-1, 2, 64)
+    v = kv[:, 128:].view(-1, 2, 64)
+    got = host(ops.dca_attention(dev_bf16(case.q), k, v, dev_i32(case.cand_offsets),
+                                 dev_i32(case.kv_offsets)))
+    assert_close(got, _want(case), "strided kv")
+
+
+def test_general_path_fp32_and_small_head(gpu_lib):
+    case = wl.attention_case([64, 64, 64, 64], [32, 32, 32, 32], 2, 32, seed=13, bf16=False)
+    got = host(ops.dca_attention(dev_f32(case.q), dev_f32(case.k), dev_f32(case.v),
+                                 dev_i32(case.cand_offsets), dev_i32(case.kv_offsets)))
+    want = ikbo.dca_attention(case.q, case.k, case.v, case.cand_offsets, case.kv_offsets)
+    assert_close(got, want, "fp32 d32", atol=1e-4, rtol=1e-4, normwise=1e-5)
+    c16 = wl.attention_case([10, 0, 33], [7, 9, 0], 3, 40, seed=14)     # d = 40: general bf16
+    assert_close(_attn(c16), _want(c16), "bf16 d40")
+
+
+def test_deterministic_and_candidate_isolation(gpu_lib):
+    case = wl.attention_case([500, 20], [300, 77], 2, 128, seed=15)
+    a = _attn(case)
+    np.testing.assert_array_equal(a, _attn(case))
+    case.q = case.q.copy()
+    case.q[7] = -case.q[7]
+    b = _attn(case)
+    keep = np.arange(a.shape[0]) != 7
+    np.testing.assert_array_equal(a[keep], b[keep])

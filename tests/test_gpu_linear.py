@@ -1,0 +1,113 @@
+"""GPU parity: rocs_ikbo_linear against the oracle (broadcast-then-compute)."""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import assert_close, dev_bf16, dev_f32, dev_i32, host
+from oracle import ikbo
+from oracle.bf16 import round_bf16
+from paper_2607_27744_amd import ops
+from paper_2607_27744_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+# (counts per request, k_req, k_cand, d_out): ragged candidate tails, K not a
+# multiple of the 32-wide MFMA step, D not a tile multiple, empty requests,
+# several requests inside one tile, and one case big enough for the large tile.
+CASES = [
+    ([300, 0, 1, 211, 17], 96, 64, 160),
+    ([1], 8, 8, 4),
+    ([129], 40, 24, 132),
+    ([3, 5, 0, 0, 7, 2, 100, 1], 1024, 256, 512),
+    ([20000, 13000, 17001], 256, 128, 516),
+]
+
+
+def _run(case, act="relu"):
+    out = ops.ikbo_linear(
+        dev_bf16(case.x_cand), dev_bf16(case.w_cand), x_req=dev_bf16(case.x_req),
+        w_req=dev_bf16(case.w_req), cand_offsets=dev_i32(case.cand_offsets), activation=act,
+        bias=None if case.bias is None else dev_f32(case.bias),
+        x_cand_add=None if case.x_cand_add is None else dev_bf16(case.x_cand_add))
+    return host(out)
+
+
+def _want(case, act):
+    xc = case.x_cand
+    if case.x_cand_add is not None:
+        xc = round_bf16(np.asarray(xc, np.float64) + case.x_cand_add)
+    return round_bf16(ikbo.ikbo_linear(case.x_req, xc, case.w_req, case.w_cand, case.bias,
+                                       case.cand_offsets, act))
+
+
+@pytest.mark.parametrize("shape", CASES, ids=lambda s: f"R{len(s[0])}-N{sum(s[0])}-kr{s[1]}-kc{s[2]}-d{s[3]}")
+@pytest.mark.parametrize("act", ["relu", "none"])
+def test_ikbo_linear_parity(gpu_lib, shape, act):
+    counts, kr, kc, d = shape
+    case = wl.linear_case(counts, kr, kc, d, seed=len(counts) + d)
+    assert_close(_run(case, act), _want(case, act), f"ikbo_linear {shape} {act}")
+
+
+def test_bias_and_residual(gpu_lib):
+    case = wl.linear_case([70, 0, 300], 64, 96, 200, seed=4, bias_std=0.5, add_residual=True)
+    assert_close(_run(case, "relu"), _want(case, "relu"), "bias + residual")
+
+
+def test_plain_linear(gpu_lib):
+    case = wl.linear_case([777], 0, 512, 256, seed=5)
+    got = host(gpu_lib.ikbo_linear(dev_bf16(case.x_cand), dev_bf16(case.w_cand)))
+    assert_close(got, round_bf16(ikbo.linear(case.x_cand, case.w_cand)), "plain")
+
+
+def test_index_probe_bit_exact(gpu_lib):
+    # x_req[r, :] = r, W_CR = e_0 on output 0, W_CC = 0: output 0 is m_n exactly.
+    counts = np.array([5, 0, 300, 1, 0, 256, 77])
+    off = wl.offsets_from_counts(counts)
+    n, r = int(counts.sum()), counts.size
+    x_req = np.repeat(np.arange(r, dtype=np.float32)[:, None], 16, axis=1)
+    w_req = np.zeros((8, 16), np.float32); w_req[0, 0] = 1.0
+    out = gpu_lib.ikbo_linear(dev_bf16(np.ones((n, 8), np.float32)), dev_bf16(np.zeros((8, 8), np.float32)),
+                              x_req=dev_bf16(x_req), w_req=dev_bf16(w_req),
+                              cand_offsets=dev_i32(off))
+    np.testing.assert_array_equal(host(out)[:, 0], np.repeat(np.arange(r), counts))
+    ids = gpu_lib.request_ids(dev_i32(off), n)
+    np.testing.assert_array_equal(ids.cpu().numpy(), ikbo.request_ids(off))
+
+
+def test_general_path_unaligned_and_fp32(gpu_lib):
+    # K = 13 is not a multiple of 8: the general kernel runs.
+    case = wl.linear_case([9, 0, 40], 13, 5, 7, seed=6)
+    assert_close(_run(case, "relu"), _want(case, "relu"), "unaligned bf16")
+    c32 = wl.linear_case([64, 64, 64, 64], 256, 128, 256, seed=7, bf16=False)
+    got = host(gpu_lib.ikbo_linear(dev_f32(c32.x_cand), dev_f32(c32.w_cand),
+                                   x_req=dev_f32(c32.x_req), w_req=dev_f32(c32.w_req),
+                                   cand_offsets=dev_i32(c32.cand_offsets), activation="relu"))
+    want = ikbo.ikbo_linear(c32.x_req, c32.x_cand, c32.w_req, c32.w_cand, None,
+                            c32.cand_offsets, "relu")
+    assert_close(got, want, "fp32")
+    assert_close(got, want, "fp32 tight", atol=1e-4, rtol=1e-4, normwise=1e-5)
+
+
+def test_deterministic_and_candidate_isolation(gpu_lib):
+    case = wl.linear_case([400, 3, 900], 128, 64, 256, seed=8)
+    a = _run(case)
+    b = _run(case)
+    np.testing.assert_array_equal(a, b)
+    # GLM invariant on the device: changing one candidate changes only its row.
+    case.x_cand = case.x_cand.copy()
+    case.x_cand[401] = -case.x_cand[401]
+    c = _run(case)
+    keep = np.arange(a.shape[0]) != 401
+    np.testing.assert_array_equal(a[keep], c[keep])
+    assert not np.array_equal(a[401], c[401])
+
+
+def test_empty_batch_is_noop(gpu_lib):
+    out = torch.full((0, 8), 7.0, device="cuda", dtype=torch.bfloat16)
+    gpu_lib.ikbo_linear(torch.empty((0, 8), device="cuda", dtype=torch.bfloat16),
+                        dev_bf16(np.zeros((8, 8), np.float32)),
+                        x_req=dev_bf16(np.zeros((2, 8), np.float32)),
+                        w_req=dev_bf16(np.zeros((8, 8), np.float32)),
+                        cand_offsets=dev_i32([0, 0, 0]), out=out)
+    assert out.numel() == 0
