@@ -21,49 +21,64 @@
 #include "kernels.h"
 #include "launch.h"
 
+#include <type_traits>
+
 namespace rocs {
 namespace {
 
-constexpr int kTileRows = 256;   // query rows per workgroup (4 waves x 64)
+constexpr int kTileRows = 256;   // query rows per workgroup (8 waves x 32)
 constexpr int kTileKeys = 64;    // history rows per K/V stage
 constexpr float kLazyRescale = 8.0f;   // log2 of the largest unnormalised weight
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA kernel, head_dim D in {64, 128}.
+// bf16 MFMA kernel (32x32x16 shape), head_dim D in {64, 128}.
+//
+// Workgroup: 8 waves x 32 query rows = one 256-row tile. With 32 rows a wave
+// needs under 256 VGPRs, so two waves share each SIMD and one wave's softmax
+// (VALU) overlaps the other's matrix-core work.
 //
 // Scores are computed transposed, S^T = K Q^T (A = K rows from LDS, B = the
-// wave's query rows held in registers for the whole history), so a lane's
-// accumulator quads hold 4 keys of one query row: the row max needs only a
-// reduction over the four 16-lane rows of the wave. O^T = V^T P^T reuses the
-// probabilities straight from registers as the B operand (the key order
-// inside one 32-key MFMA step is a fixed permutation applied to both P and
+// wave's query rows held in registers for the whole history), so each lane's
+// accumulator holds 16 keys of one query row: the row max needs only one
+// exchange between the two wave halves. O^T = V^T P^T reuses the
+// probabilities straight from registers as the B operand (the order of the
+// 16 keys inside one MFMA step is a fixed permutation applied to both P and
 // V^T), so V is stored transposed in LDS.
 //
 // Online softmax in the exp2 domain, scale * log2(e) folded into one FMA.
-// The running max is only moved when a tile's max exceeds it by more than
-// 2^kLazyRescale, so the accumulator rescale is skipped for almost every tile
-// (unnormalised weights stay below 2^8; the final division by the row sum is
-// exact in the algebra). Row sums are accumulated per 16-lane row from the
-// bf16-rounded weights the PV product uses, and reduced once at the end.
+// The running max is only moved when a stage's max exceeds it by more than
+// 2^kLazyRescale, so the accumulator rescale is skipped for almost every
+// stage (unnormalised weights stay below 2^8; the final division by the row
+// sum is exact in the algebra). Row sums are accumulated per wave half from
+// the bf16-rounded weights the PV product uses, and combined at the end.
+//
+// Loads never branch: history and query row indices are clamped into range,
+// and the keys past the history's end are masked (weight 0) in the last,
+// ragged stage only.
 // ---------------------------------------------------------------------------
+constexpr int kAttnWaves = 8;
+
 template <int D>
-__global__ __launch_bounds__(256) void dca_attn_bf16(
+__global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
     int64_t slots_per_head) {
-  constexpr int RB = 4;               // 16-row blocks per wave
-  constexpr int KS = D / 32;          // MFMA steps over head_dim
-  constexpr int DB = D / 16;          // 16-wide output column blocks
+  constexpr int NT = 64 * kAttnWaves;
+  constexpr int KB = kTileKeys / 32;  // 32-key blocks per stage
+  constexpr int KS = D / 16;          // MFMA steps over head_dim
+  constexpr int DB = D / 32;          // 32-wide output column blocks
+  constexpr int PS = kTileKeys / 16;  // MFMA steps over the stage's keys
   constexpr int KROW = D + 8;         // K stage row: 16-byte pad
   constexpr int VROW = kTileKeys + 4; // V^T stage row: 8-byte pad
-  constexpr int KCH = kTileKeys * D / 8 / 256;     // 16-byte K chunks per thread
+  constexpr int KCH = kTileKeys * D / 8 / NT;       // 16-byte K chunks per thread
   constexpr int VUNITS = (kTileKeys / 4) * (D / 8); // (4 keys x 8 dims) V units
+  static_assert(KCH >= 1 && VUNITS <= NT, "staging does not tile");
   __shared__ __attribute__((aligned(16))) bf16_t lds_k[2][kTileKeys][KROW];
   __shared__ __attribute__((aligned(16))) bf16_t lds_v[2][D][VROW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 15, g = lane >> 4;
+  const int l32 = lane & 31, hh = lane >> 5;
   const uint32_t work = xcd_remap(blockIdx.x, gridDim.x);
   const int h = (int)(work / (uint64_t)slots_per_head);
   const int64_t slot = (int64_t)(work % (uint64_t)slots_per_head);
@@ -80,193 +95,199 @@ __global__ __launch_bounds__(256) void dca_attn_bf16(
   bf16_t* oh = out + row0 * qs + (int64_t)h * D;
 
   if (L == 0) {                                           // empty history: zeros
-    for (int c = tid; c < rows * (D / 8); c += 256) {
+    for (int c = tid; c < rows * (D / 8); c += NT) {
       const int rr = c / (D / 8), dc = (c % (D / 8)) * 8;
       *reinterpret_cast<u32x4*>(oh + rr * qs + dc) = u32x4{0u, 0u, 0u, 0u};
     }
     return;
   }
 
-  // This wave's query rows, as B fragments: lane holds Q[row lr][8g .. 8g+7]
-  // of each 16-row block and 32-wide head_dim step.
-  const int wrow0 = wave * 64;
+  // This wave's 32 query rows as B fragments: lane holds Q[row l32][16 ks + 8 hh .. +7].
+  const int wrow0 = wave * 32;
   const bool active = wrow0 < rows;
-  bf16x8 qf[RB][KS];
+  const int qrow = min(wrow0 + l32, rows - 1);            // clamped; extra rows never stored
+  bf16x8 qf[KS];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int rr = wrow0 + 16 * rb + lr;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[rb][ks] = as_bf16x8(load16(qh + rr * qs + 32 * ks + 8 * g, rr < rows));
-  }
+  for (int ks = 0; ks < KS; ++ks)
+    qf[ks] = *reinterpret_cast<const bf16x8*>(qh + qrow * qs + 16 * ks + 8 * hh);
 
   // K/V staging. K: chunk c -> key c / (D/8), dims (c % (D/8)) * 8.
   // V: unit u -> keys 4 (u % 16) .. +3, dims (u / 16) * 8 .. +7, written
-  // transposed as eight 4-key rows.
+  // transposed as eight 4-key rows. Each thread keeps pointers to its rows of
+  // stage 0 and adds the stage offset; only the last stage clamps key
+  // indices to L - 1.
   const bf16_t* kh = k + kv0 * kv_stride + (int64_t)h * D;
   const bf16_t* vh = v + kv0 * kv_stride + (int64_t)h * D;
+  const bool has_v = tid < VUNITS;
+  const int vkg = tid % 16, vdc = (tid / 16) * 8;
+  const bf16_t* kp[KCH];
+  int kkey[KCH];
+#pragma unroll
+  for (int i = 0; i < KCH; ++i) {
+    const int c = tid + NT * i;
+    kkey[i] = c / (D / 8);
+    kp[i] = kh + (int64_t)kkey[i] * kv_stride + (c % (D / 8)) * 8;
+  }
+  const bf16_t* vp = vh + (int64_t)(4 * vkg) * kv_stride + vdc;
   u32x4 rk[KCH], rv[4];
   auto load_kv = [&](int base) {
+    const int64_t off = (int64_t)base * kv_stride;
+    if (base + kTileKeys <= L) {
 #pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + 256 * i, key = c / (D / 8), dc = (c % (D / 8)) * 8;
-      rk[i] = load16(kh + (int64_t)(base + key) * kv_stride + dc, base + key < L);
-    }
-    if (tid < VUNITS) {
-      const int kg = tid % 16, dc = (tid / 16) * 8;
+      for (int i = 0; i < KCH; ++i) rk[i] = *reinterpret_cast<const u32x4*>(kp[i] + off);
+      if (has_v) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = base + 4 * kg + e;
-        rv[e] = load16(vh + (int64_t)key * kv_stride + dc, key < L);
+        for (int e = 0; e < 4; ++e)
+          rv[e] = *reinterpret_cast<const u32x4*>(vp + off + (int64_t)e * kv_stride);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < KCH; ++i) {
+        const int key = min(base + kkey[i], L - 1) - kkey[i];
+        rk[i] = *reinterpret_cast<const u32x4*>(kp[i] + (int64_t)key * kv_stride);
+      }
+      if (has_v) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = min(base + 4 * vkg + e, L - 1) - 4 * vkg;
+          rv[e] = *reinterpret_cast<const u32x4*>(vp + (int64_t)key * kv_stride);
+        }
       }
     }
   };
   auto store_kv = [&](int buf) {
 #pragma unroll
     for (int i = 0; i < KCH; ++i) {
-      const int c = tid + 256 * i, key = c / (D / 8), dc = (c % (D / 8)) * 8;
-      *reinterpret_cast<u32x4*>(&lds_k[buf][key][dc]) = rk[i];
+      const int c = tid + NT * i;
+      *reinterpret_cast<u32x4*>(&lds_k[buf][kkey[i]][(c % (D / 8)) * 8]) = rk[i];
     }
-    if (tid < VUNITS) {
-      const int kg = tid % 16, dc = (tid / 16) * 8;
+    if (has_v) {
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        // dims dc + 2w (low halves) and dc + 2w + 1 (high halves)
-        const u32x2 lo = {(rv[0][w] & 0xffffu) | (rv[1][w] << 16),
-                          (rv[2][w] & 0xffffu) | (rv[3][w] << 16)};
-        const u32x2 hi = {(rv[0][w] >> 16) | (rv[1][w] & 0xffff0000u),
-                          (rv[2][w] >> 16) | (rv[3][w] & 0xffff0000u)};
-        *reinterpret_cast<u32x2*>(&lds_v[buf][dc + 2 * w][4 * kg]) = lo;
-        *reinterpret_cast<u32x2*>(&lds_v[buf][dc + 2 * w + 1][4 * kg]) = hi;
+        // dims vdc + 2w (low halves of the four keys) and vdc + 2w + 1 (high halves)
+        const u32x2 lo = {__builtin_amdgcn_perm(rv[1][w], rv[0][w], 0x05040100u),
+                          __builtin_amdgcn_perm(rv[3][w], rv[2][w], 0x05040100u)};
+        const u32x2 hi = {__builtin_amdgcn_perm(rv[1][w], rv[0][w], 0x07060302u),
+                          __builtin_amdgcn_perm(rv[3][w], rv[2][w], 0x07060302u)};
+        *reinterpret_cast<u32x2*>(&lds_v[buf][vdc + 2 * w][4 * vkg]) = lo;
+        *reinterpret_cast<u32x2*>(&lds_v[buf][vdc + 2 * w + 1][4 * vkg]) = hi;
       }
     }
   };
 
-  float m_run[RB], l_part[RB];
-  f32x4 oacc[DB][RB];
+  float m_run = -INFINITY, l_part = 0.f;
+  f32x16 oacc[DB];
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    m_run[rb] = -INFINITY;
-    l_part[rb] = 0.f;
+  for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int db = 0; db < DB; ++db) oacc[db][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+    for (int e = 0; e < 16; ++e) oacc[db][e] = 0.f;
+
+  // One stage of 64 keys from LDS buffer `cur`; `valid` keys are real (the
+  // rest of a ragged last stage gets weight 0).
+  auto stage = [&](int cur, auto masked, int valid) {
+    // S^T: element 4 qq + i of sacc[kb] is S[key 32 kb + 8 qq + 4 hh + i][row l32]
+    f32x16 sacc[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lds_k[cur][32 * kb + l32][16 * ks + 8 * hh]);
+        sacc[kb] = mfma32(a, qf[ks], sacc[kb]);
+      }
+      // Keep at most two steps of K fragments in flight (register budget for
+      // two waves per SIMD); the other wave on the SIMD covers the latency.
+      if (ks % 2 == 1) __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (decltype(masked)::value) {              // the last stage only
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (32 * kb + 8 * (e / 4) + 4 * hh + (e % 4) >= valid) sacc[kb][e] = -INFINITY;
+    }
+    // Row max: 32 keys per lane, then across the two wave halves.
+    float mx = sacc[0][0];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sacc[kb][e]);
+    mx = max_across_halves(mx) * scale_log2;
+    const bool need = mx > m_run + kLazyRescale;
+    if (__ballot(need) != 0) {
+      const float m_new = need ? mx : m_run;
+      const float alpha = exp2f(m_run - m_new);            // 0 on the first stage
+      m_run = m_new;
+      l_part *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+    }
+    // Probabilities (bf16) as B fragments of the PV product. MFMA step ps
+    // covers keys 16 ps + 4 hh + {0..3} and 16 ps + 8 + 4 hh + {0..3}:
+    // elements 8 (ps % 2) .. +7 of sacc[ps / 2].
+    const bf16x2 ones = {(bf16_t)1.0f, (bf16_t)1.0f};
+#pragma unroll
+    for (int ps = 0; ps < PS; ++ps) {
+      // Each packed pair is a scalar of its own: the row-sum dot2 must not
+      // read its operand out of a vector register tuple (the gfx950 code
+      // generator has been seen to feed the same tuple element to every dot2
+      // in that form).
+      uint32_t pk[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float s0 = sacc[ps / 2][8 * (ps % 2) + 2 * w];
+        const float s1 = sacc[ps / 2][8 * (ps % 2) + 2 * w + 1];
+        pk[w] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(s0, scale_log2, -m_run)),
+                            __builtin_amdgcn_exp2f(fmaf(s1, scale_log2, -m_run)));
+        l_part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[w]), ones, l_part,
+                                                 false);
+      }
+      const bf16x8 pf = as_bf16x8(u32x4{pk[0], pk[1], pk[2], pk[3]});
+      // O^T += V^T P^T: A lane holds V^T[32 db + l32][the same 8 keys].
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[cur][32 * db + l32][16 * ps + 4 * hh]);
+        const u32x2 hi =
+            *reinterpret_cast<const u32x2*>(&lds_v[cur][32 * db + l32][16 * ps + 8 + 4 * hh]);
+        oacc[db] = mfma32(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pf, oacc[db]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
 
   const int ntiles = (L + kTileKeys - 1) / kTileKeys;
+  const int last_valid = L - (ntiles - 1) * kTileKeys;    // keys in the last stage
   load_kv(0);
   store_kv(0);
   __syncthreads();
-  for (int kt = 0; kt < ntiles; ++kt) {
+  // Full stages; the last (possibly ragged) stage is peeled off below so the
+  // loop body carries no masking code.
+  for (int kt = 0; kt + 1 < ntiles; ++kt) {
     const int cur = kt & 1;
-    const int base = kt * kTileKeys;
-    if (kt + 1 < ntiles) load_kv(base + kTileKeys);
-    if (active) {
-      // S^T: sacc[kb][rb][i] = S[key 16 kb + 4 g + i][row 16 rb + lr]
-      f32x4 sacc[4][RB];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) sacc[kb][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8*>(&lds_k[cur][16 * kb + lr][32 * ks + 8 * g]);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) sacc[kb][rb] = mfma16(a, qf[rb][ks], sacc[kb][rb]);
-        }
-      }
-      if (base + kTileKeys > L) {                         // ragged last tile
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (base + 16 * kb + 4 * g + i >= L)
-#pragma unroll
-              for (int rb = 0; rb < RB; ++rb) sacc[kb][rb][i] = -INFINITY;
-      }
-      // Row max (lane-local over 16 keys, then over the four 16-lane rows).
-      float m_new[RB];
-      bool need = false;
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        float mx = sacc[0][rb][0];
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, sacc[kb][rb][i]);
-        mx = max_across_rows(mx) * scale_log2;
-        m_new[rb] = mx > m_run[rb] + kLazyRescale ? mx : m_run[rb];
-        need |= m_new[rb] != m_run[rb];
-      }
-      if (__ballot(need) != 0) {
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          const float alpha = exp2f(m_run[rb] - m_new[rb]);   // 0 on the first tile
-          m_run[rb] = m_new[rb];
-          l_part[rb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < DB; ++db) oacc[db][rb] *= alpha;
-        }
-      }
-      // Probabilities (bf16) as B fragments of the PV product: 32-key step
-      // ks2 uses keys 32 ks2 + 4 g + {0..3} and 32 ks2 + 16 + 4 g + {0..3}.
-      bf16x8 pf[2][RB];
-      const bf16x2 ones = {(bf16_t)1.0f, (bf16_t)1.0f};
-#pragma unroll
-      for (int ks2 = 0; ks2 < 2; ++ks2)
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-          u32x4 pk;
-#pragma unroll
-          for (int half = 0; half < 2; ++half) {
-            const f32x4 s = sacc[2 * ks2 + half][rb];
-            const float mr = m_run[rb];
-            const uint32_t p01 = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(s[0], scale_log2, -mr)),
-                                             __builtin_amdgcn_exp2f(fmaf(s[1], scale_log2, -mr)));
-            const uint32_t p23 = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(s[2], scale_log2, -mr)),
-                                             __builtin_amdgcn_exp2f(fmaf(s[3], scale_log2, -mr)));
-            pk[2 * half] = p01;
-            pk[2 * half + 1] = p23;
-            l_part[rb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p01), ones,
-                                                         l_part[rb], false);
-            l_part[rb] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p23), ones,
-                                                         l_part[rb], false);
-          }
-          pf[ks2][rb] = as_bf16x8(pk);
-        }
-      // O^T += V^T P^T: A lane holds V^T[16 db + lr][the same 8 keys].
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[cur][16 * db + lr][32 * ks2 + 4 * g]);
-          const u32x2 hi =
-              *reinterpret_cast<const u32x2*>(&lds_v[cur][16 * db + lr][32 * ks2 + 16 + 4 * g]);
-          const bf16x8 a = as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]});
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb) oacc[db][rb] = mfma16(a, pf[ks2][rb], oacc[db][rb]);
-        }
-    }
-    if (kt + 1 < ntiles) store_kv(cur ^ 1);
+    load_kv((kt + 1) * kTileKeys);
+    if (active) stage(cur, std::false_type(), kTileKeys);
+    store_kv(cur ^ 1);
     __syncthreads();
   }
+  if (active) stage((ntiles - 1) & 1, std::true_type(), last_valid);
 
   if (!active) return;
-  // oacc[db][rb][i] = O[row 16 rb + lr][dim 16 db + 4 g + i]
+  // Element 4 qq + i of oacc[db] is O[row l32][dim 32 db + 8 qq + 4 hh + i].
+  const float inv = 1.0f / sum_across_halves(l_part);
+  const int rr = wrow0 + l32;
+  if (rr >= rows) return;
 #pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const float inv = 1.0f / sum_across_rows(l_part[rb]);
-    const int rr = wrow0 + 16 * rb + lr;
-    if (rr >= rows) continue;
+  for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const f32x4 o = oacc[db][rb] * inv;
-      *reinterpret_cast<u32x2*>(oh + rr * qs + 16 * db + 4 * g) =
-          u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+    for (int qq = 0; qq < 4; ++qq) {
+      const f32x16& o = oacc[db];
+      *reinterpret_cast<u32x2*>(oh + rr * qs + 32 * db + 8 * qq + 4 * hh) =
+          u32x2{pack_bf16x2(o[4 * qq] * inv, o[4 * qq + 1] * inv),
+                pack_bf16x2(o[4 * qq + 2] * inv, o[4 * qq + 3] * inv)};
     }
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -327,7 +348,7 @@ hipError_t launch_fast(const AttentionArgs& a, hipStream_t s) {
   const int64_t slots = a.R + (a.N * a.q_len + kTileRows - 1) / kTileRows;
   const int64_t grid = slots * a.heads;
   const float scale_log2 = a.scale * 1.4426950408889634f;
-  return launch_kernel(dca_attn_bf16<D>, dim3((uint32_t)grid), dim3(256), s,
+  return launch_kernel(dca_attn_bf16<D>, dim3((uint32_t)grid), dim3(64 * kAttnWaves), s,
                        static_cast<const bf16_t*>(a.q), static_cast<const bf16_t*>(a.k),
                        static_cast<const bf16_t*>(a.v), a.cand_offsets, a.kv_offsets,
                        static_cast<bf16_t*>(a.out), (int)a.R, a.q_len, a.heads, a.kv_stride,

@@ -70,15 +70,15 @@ __global__ __launch_bounds__(256) void request_gemm_bf16(
 }
 
 // ---------------------------------------------------------------------------
-// Candidate-side GEMM with the fused request broadcast, bf16 MFMA.
+// Candidate-side GEMM with the fused request broadcast, bf16 MFMA 32x32x16.
 //
 // Matrix-core roles: A = W_CC rows (output features d), B = candidate rows,
-// so each lane's accumulator quad holds 4 consecutive output features of one
-// candidate (an 8-byte bf16 store). Workgroup tile BM (features) x BN
-// (candidates), WAVES_M x WAVES_N waves, K staged through double-buffered
-// LDS in BK-wide slabs; the next slab is prefetched into registers while the
-// current one feeds the MFMAs. LDS rows carry a 16-byte pad so the 16 rows
-// read by one fragment load fall on distinct banks.
+// so each lane's accumulator holds, for one candidate, four runs of 4
+// consecutive output features (8-byte bf16 stores). Workgroup tile BM
+// (features) x BN (candidates), WAVES_M x WAVES_N waves, K staged through
+// double-buffered LDS in BK-wide slabs; the next slab is prefetched into
+// registers while the current one feeds the MFMAs. LDS rows carry a 16-byte
+// pad so the rows read by one fragment load spread over all banks.
 //
 // Epilogue fusion: accumulators are initialised with Z[m_n][d] + b[d] before
 // the K loop (so these loads overlap the first slab's loads), and the
@@ -94,12 +94,13 @@ void ikbo_gemm_bf16(
     bf16_t* __restrict__ out, int64_t N, int K, int D, int tiles_m, int relu) {
   constexpr int NT = 64 * WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
-  constexpr int FM = WM / 16, FN = WN / 16;
+  constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int ROW = BK + 8;                 // LDS row (bf16) with 16-byte pad
   constexpr int CPR = BK / 8;                 // 16-byte chunks per slab row
   constexpr int RPP = NT / CPR;               // slab rows staged per pass
   constexpr int CA = BM / RPP, CB = BN / RPP;
   static_assert(BM % RPP == 0 && BN % RPP == 0, "staging does not tile");
+  static_assert(WM % 32 == 0 && WN % 32 == 0 && BK % 16 == 0, "MFMA tiling");
   __shared__ __attribute__((aligned(16))) bf16_t lds_a[2][BM][ROW];
   __shared__ __attribute__((aligned(16))) bf16_t lds_b[2][BN][ROW];
 
@@ -108,7 +109,7 @@ void ikbo_gemm_bf16(
   const int m0 = (int)(tile % (uint32_t)tiles_m) * BM;
   const int64_t n0 = (int64_t)(tile / (uint32_t)tiles_m) * BN;
   const int wm0 = (wave % WAVES_M) * WM, wn0 = (wave / WAVES_M) * WN;
-  const int lr = lane & 15, g4 = (lane >> 4) * 4, g8 = (lane >> 4) * 8;
+  const int l32 = lane & 31, h4 = (lane >> 5) * 4, h8 = (lane >> 5) * 8;
 
   const int srow = tid / CPR, skc = (tid % CPR) * 8;
   u32x4 ra[CA], rb[CB];
@@ -149,49 +150,32 @@ void ikbo_gemm_bf16(
   const int nk = (K + BK - 1) / BK;
   load_slab(0);
 
-  // Accumulators start at b[d] + Z[m_n][d].
-  f32x4 acc[FM][FN];
+  // Accumulators start at b[d] + Z[m_n][d]; element 4 q + i of tile (fm, fn)
+  // is feature m0 + wm0 + 32 fm + 8 q + h4 + i of candidate n0 + wn0 + 32 fn + l32.
+  f32x16 acc[FM][FN];
   {
-    f32x4 bv[FM];
+    const bool one_request = z != nullptr && ids[n0] == ids[(n0 + BN < N ? n0 + BN : N) - 1];
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const int d = m0 + wm0 + 16 * fm + g4;
-      const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-      bv[fm] = (bias != nullptr && d < D) ? *reinterpret_cast<const f32x4*>(bias + d) : zero;
-    }
-    if (z != nullptr) {
-      const int64_t nlast = (n0 + BN < N ? n0 + BN : N) - 1;
-      const int rfirst = ids[n0], rlast = ids[nlast];
-      if (rfirst == rlast) {
-        const float* zr = z + (int64_t)rfirst * D;
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm) {
-          const int d = m0 + wm0 + 16 * fm + g4;
-          f32x4 zv = {0.f, 0.f, 0.f, 0.f};
-          if (d < D) zv = *reinterpret_cast<const f32x4*>(zr + d);
-#pragma unroll
-          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = zv + bv[fm];
-        }
-      } else {
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          const int64_t n = n0 + wn0 + 16 * fn + lr;
-          const int r = n < N ? ids[n] : 0;
-          const float* zr = z + (int64_t)r * D;
-#pragma unroll
-          for (int fm = 0; fm < FM; ++fm) {
-            const int d = m0 + wm0 + 16 * fm + g4;
-            f32x4 zv = {0.f, 0.f, 0.f, 0.f};
-            if (d < D && n < N) zv = *reinterpret_cast<const f32x4*>(zr + d);
-            acc[fm][fn] = zv + bv[fm];
-          }
-        }
+    for (int fn = 0; fn < FN; ++fn) {
+      const int64_t n = n0 + wn0 + 32 * fn + l32;
+      const float* zr = nullptr;
+      if (z != nullptr) {
+        const int r = one_request ? ids[n0] : (n < N ? ids[n] : 0);
+        zr = z + (int64_t)r * D;
       }
-    } else {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = bv[fm];
+        for (int q = 0; q < 4; ++q) {
+          const int d = m0 + wm0 + 32 * fm + 8 * q + h4;
+          f32x4 v = {0.f, 0.f, 0.f, 0.f};
+          if (d < D) {
+            if (bias != nullptr) v = *reinterpret_cast<const f32x4*>(bias + d);
+            if (zr != nullptr && (one_request || n < N)) v += *reinterpret_cast<const f32x4*>(zr + d);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[fm][fn][4 * q + i] = v[i];
+        }
     }
   }
 
@@ -201,18 +185,18 @@ void ikbo_gemm_bf16(
     const int cur = kt & 1;
     if (kt + 1 < nk) load_slab((kt + 1) * BK);
 #pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
+    for (int ks = 0; ks < BK / 16; ++ks) {
       bf16x8 af[FM], bfr[FN];
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
-        af[fm] = *reinterpret_cast<const bf16x8*>(&lds_a[cur][wm0 + 16 * fm + lr][ks * 32 + g8]);
+        af[fm] = *reinterpret_cast<const bf16x8*>(&lds_a[cur][wm0 + 32 * fm + l32][ks * 16 + h8]);
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn)
-        bfr[fn] = *reinterpret_cast<const bf16x8*>(&lds_b[cur][wn0 + 16 * fn + lr][ks * 32 + g8]);
+        bfr[fn] = *reinterpret_cast<const bf16x8*>(&lds_b[cur][wn0 + 32 * fn + l32][ks * 16 + h8]);
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma16(af[fm], bfr[fn], acc[fm][fn]);
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[fm], bfr[fn], acc[fm][fn]);
     }
     if (kt + 1 < nk) store_slab(cur ^ 1);
     __syncthreads();
@@ -221,20 +205,20 @@ void ikbo_gemm_bf16(
   // Epilogue: activation, round to bf16, 8-byte stores.
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
-    const int64_t n = n0 + wn0 + 16 * fn + lr;
+    const int64_t n = n0 + wn0 + 32 * fn + l32;
     if (n >= N) continue;
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const int d = m0 + wm0 + 16 * fm + g4;
-      if (d >= D) continue;
-      f32x4 v = acc[fm][fn];
-      if (relu) {
+    for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = fmaxf(v[i], 0.f);
+      for (int q = 0; q < 4; ++q) {
+        const int d = m0 + wm0 + 32 * fm + 8 * q + h4;
+        if (d >= D) continue;
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = relu ? fmaxf(acc[fm][fn][4 * q + i], 0.f) : acc[fm][fn][4 * q + i];
+        *reinterpret_cast<u32x2*>(out + n * D + d) =
+            u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
       }
-      const u32x2 pk = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-      *reinterpret_cast<u32x2*>(out + n * D + d) = pk;
-    }
   }
 }
 
