@@ -148,6 +148,25 @@ def timed_step_fns(p):
     raise ValueError(cid)
 
 
+_OP_KERNEL = (("dca_attention", "dca_attn_bf16"), ("glm_interaction", "glm_fm_bf16"),
+              ("", "ikbo_gemm_bf16"))
+
+
+def profiled_traffic(workload, op):
+    """HBM bytes per launch from a committed rocprofv3 summary, or None when
+    there is none or the kernel's source has changed since it was taken."""
+    from paper_2607_27744_amd import prof_summary
+    path = os.path.join(_ROOT, "profiles", f"traffic_workload{workload}_{op}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    key = next(k for prefix, k in _OP_KERNEL if op.startswith(prefix))
+    if rec.get("source_sha256") != prof_summary.source_hash(key):
+        return None
+    return rec["hbm_bytes_per_launch"]
+
+
 def cpu_baseline(w, cid):
     """The oracle, as it stands, on a bounded sample of the workload."""
     import numpy as np
@@ -254,7 +273,8 @@ def main():
     else:
         achieved, peak, unit = flops / (op_ms[dom] * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
     roofline = {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None}
+                "unit": unit, "frac": round(achieved / peak, 4),
+                "traffic": profiled_traffic(args.workload, name)}
 
     cpu = None
     if not args.no_cpu_baseline:

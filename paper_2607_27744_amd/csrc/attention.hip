@@ -57,6 +57,7 @@ constexpr float kLazyRescale = 8.0f;   // log2 of the largest unnormalised weigh
 // ragged stage only.
 // ---------------------------------------------------------------------------
 constexpr int kAttnWaves = 8;
+constexpr int kStages = 3;       // K/V ring buffer depth in LDS
 
 template <int D>
 __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
@@ -74,8 +75,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
   constexpr int KCH = kTileKeys * D / 8 / NT;       // 16-byte K chunks per thread
   constexpr int VUNITS = (kTileKeys / 4) * (D / 8); // (4 keys x 8 dims) V units
   static_assert(KCH >= 1 && VUNITS <= NT, "staging does not tile");
-  __shared__ __attribute__((aligned(16))) bf16_t lds_k[2][kTileKeys][KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t lds_v[2][D][VROW];
+  __shared__ __attribute__((aligned(16))) bf16_t lds_k[kStages][kTileKeys][KROW];
+  __shared__ __attribute__((aligned(16))) bf16_t lds_v[kStages][D][VROW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
@@ -182,11 +183,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
 #pragma unroll
     for (int e = 0; e < 16; ++e) oacc[db][e] = 0.f;
 
-  // One stage of 64 keys from LDS buffer `cur`; `valid` keys are real (the
-  // rest of a ragged last stage gets weight 0).
-  auto stage = [&](int cur, auto masked, int valid) {
-    // S^T: element 4 qq + i of sacc[kb] is S[key 32 kb + 8 qq + 4 hh + i][row l32]
-    f32x16 sacc[KB];
+  // Scores of one stage: S^T for the 64 keys in LDS buffer `buf`. Element
+  // 4 qq + i of sacc[kb] is S[key 32 kb + 8 qq + 4 hh + i][row l32].
+  auto qk = [&](int buf, f32x16 (&sacc)[KB]) {
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -195,14 +194,19 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
     for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lds_k[cur][32 * kb + l32][16 * ks + 8 * hh]);
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lds_k[buf][32 * kb + l32][16 * ks + 8 * hh]);
         sacc[kb] = mfma32(a, qf[ks], sacc[kb]);
       }
       // Keep at most two steps of K fragments in flight (register budget for
       // two waves per SIMD); the other wave on the SIMD covers the latency.
       if (ks % 2 == 1) __builtin_amdgcn_sched_barrier(0);
     }
-    if constexpr (decltype(masked)::value) {              // the last stage only
+  };
+
+  // Softmax, first half: mask (last stage only), row max and the lazy
+  // rescale of the running state.
+  auto row_max = [&](f32x16 (&sacc)[KB], auto masked, int valid) {
+    if constexpr (decltype(masked)::value) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -225,6 +229,11 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
 #pragma unroll
       for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
     }
+  };
+
+  // Softmax, second half: probabilities and the PV product against the V^T
+  // in LDS buffer `buf`.
+  auto exp_pv = [&](int buf, f32x16 (&sacc)[KB]) {
     // Probabilities (bf16) as B fragments of the PV product. MFMA step ps
     // covers keys 16 ps + 4 hh + {0..3} and 16 ps + 8 + 4 hh + {0..3}:
     // elements 8 (ps % 2) .. +7 of sacc[ps / 2].
@@ -249,30 +258,59 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
       // O^T += V^T P^T: A lane holds V^T[32 db + l32][the same 8 keys].
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[cur][32 * db + l32][16 * ps + 4 * hh]);
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[buf][32 * db + l32][16 * ps + 4 * hh]);
         const u32x2 hi =
-            *reinterpret_cast<const u32x2*>(&lds_v[cur][32 * db + l32][16 * ps + 8 + 4 * hh]);
+            *reinterpret_cast<const u32x2*>(&lds_v[buf][32 * db + l32][16 * ps + 8 + 4 * hh]);
         oacc[db] = mfma32(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pf, oacc[db]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
 
+  // Software pipeline over stages: while the matrix cores compute the scores
+  // of stage t + 1, the VALU runs the softmax of stage t, then stage t's PV
+  // product follows. K/V live in a 3-deep LDS ring (stages t, t + 1 and the
+  // one being filled for t + 2), so one barrier per stage suffices.
   const int ntiles = (L + kTileKeys - 1) / kTileKeys;
   const int last_valid = L - (ntiles - 1) * kTileKeys;    // keys in the last stage
   load_kv(0);
   store_kv(0);
-  __syncthreads();
-  // Full stages; the last (possibly ragged) stage is peeled off below so the
-  // loop body carries no masking code.
-  for (int kt = 0; kt + 1 < ntiles; ++kt) {
-    const int cur = kt & 1;
-    load_kv((kt + 1) * kTileKeys);
-    if (active) stage(cur, std::false_type(), kTileKeys);
-    store_kv(cur ^ 1);
-    __syncthreads();
+  if (ntiles > 1) {
+    load_kv(kTileKeys);
+    store_kv(1);
   }
-  if (active) stage((ntiles - 1) & 1, std::true_type(), last_valid);
+  __syncthreads();
+  // One pipelined step: finish the softmax bookkeeping of stage kt (scores
+  // in s_cur), start the scores of stage kt + 1 into s_next on the matrix
+  // cores, and let the VALU exponentiate stage kt meanwhile, then its PV.
+  f32x16 s_a[KB], s_b[KB];
+  auto step = [&](int kt, f32x16 (&s_cur)[KB], f32x16 (&s_next)[KB]) {
+    const bool fill = kt + 2 < ntiles;
+    if (fill) load_kv((kt + 2) * kTileKeys);
+    if (active) {
+      row_max(s_cur, std::false_type(), kTileKeys);
+      qk((kt + 1) % kStages, s_next);
+      exp_pv(kt % kStages, s_cur);
+    }
+    if (fill) store_kv((kt + 2) % kStages);
+    __syncthreads();
+  };
+  if (active) qk(0, s_a);
+  int kt = 0;
+  for (; kt + 2 < ntiles; kt += 2) {        // unrolled by two: the score buffers swap roles
+    step(kt, s_a, s_b);
+    step(kt + 1, s_b, s_a);
+  }
+  if (kt + 1 < ntiles) {
+    step(kt, s_a, s_b);
+    if (active) {
+      row_max(s_b, std::true_type(), last_valid);
+      exp_pv((ntiles - 1) % kStages, s_b);
+    }
+  } else if (active) {
+    row_max(s_a, std::true_type(), last_valid);
+    exp_pv((ntiles - 1) % kStages, s_a);
+  }
 
   if (!active) return;
   // Element 4 qq + i of oacc[db] is O[row l32][dim 32 db + 8 qq + 4 hh + i].
