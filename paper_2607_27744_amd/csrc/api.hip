@@ -191,6 +191,7 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
   a.bf16 = dtype == ROCS_DTYPE_BF16;
   a.out = out;
   const bool fast = a.bf16 && (head_dim == 64 || head_dim == 128) && stride % 8 == 0 &&
+                    stride < (int64_t(1) << 24) &&
                     aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16);
   const hipError_t e = rocs::launch_attention(a, fast, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_dca_attention: %s", hipGetErrorString(e));

@@ -28,7 +28,13 @@ namespace {
 
 constexpr int kTileRows = 256;   // query rows per workgroup (8 waves x 32)
 constexpr int kTileKeys = 64;    // history rows per K/V stage
-constexpr float kLazyRescale = 8.0f;   // log2 of the largest unnormalised weight
+// Online softmax bound: a stage's weights are kept only while their per-lane
+// sum is at most 2^64 (each weight then is too); otherwise the running max
+// moves to the stage max. Row sums stay below L * 2^64 and outputs below
+// L * 2^64 * max|v|, finite in fp32 (and in bf16, which has its exponent
+// range) for any realistic history.
+constexpr float kLazyRescale = 64.0f;     // log2 of the largest unnormalised weight
+constexpr float kWeightBound = 0x1p64f;
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel (32x32x16 shape), head_dim D in {64, 128}.
@@ -43,12 +49,20 @@ constexpr float kLazyRescale = 8.0f;   // log2 of the largest unnormalised weigh
 // exchange between the two wave halves. O^T = V^T P^T reuses the
 // probabilities straight from registers as the B operand (the order of the
 // 16 keys inside one MFMA step is a fixed permutation applied to both P and
-// V^T), so V is stored transposed in LDS.
+// V^T).
+//
+// K/V staging: history rows go from HBM/L2 straight into LDS with the DMA
+// form of the global load (no VGPR round trip, no LDS store instructions),
+// two stages ahead of use through a 4-deep ring. Rows keep their HBM layout in
+// LDS, with the 16-byte chunks of each row XOR-swizzled by the row index so
+// that both fragment reads are conflict-free; V^T fragments come out of the
+// row-major V stage through the transposing LDS read (ds_read_b64_tr_b16).
 //
 // Online softmax in the exp2 domain, scale * log2(e) folded into one FMA.
-// The running max is only moved when a stage's max exceeds it by more than
-// 2^kLazyRescale, so the accumulator rescale is skipped for almost every
-// stage (unnormalised weights stay below 2^8; the final division by the row
+// Weights are taken against the running max as it stands; the max (and the
+// accumulator rescale) is only computed when a stage's weights could pass
+// 2^kLazyRescale, which the per-lane sum of the weights detects, so after the
+// first stage almost no stage needs a row max (the final division by the row
 // sum is exact in the algebra). Row sums are accumulated per wave half from
 // the bf16-rounded weights the PV product uses, and combined at the end.
 //
@@ -57,7 +71,43 @@ constexpr float kLazyRescale = 8.0f;   // log2 of the largest unnormalised weigh
 // ragged stage only.
 // ---------------------------------------------------------------------------
 constexpr int kAttnWaves = 8;
-constexpr int kStages = 3;       // K/V ring buffer depth in LDS
+constexpr int kStages = 4;       // K/V ring depth in LDS (loads run two stages ahead)
+
+#define ROCS_LDS __attribute__((address_space(3)))
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte chunk c of history row `key` (D bf16 = 2D bytes) sits at chunk
+// position c ^ kv_swizzle(key) of its LDS row. Conflict-free for both read
+// patterns: 16 consecutive rows at one chunk (K fragments) and 4 consecutive
+// rows x 4 consecutive chunks (transposing V reads).
+template <int D>
+__device__ __forceinline__ int kv_swizzle(int key) {
+  if constexpr (D == 128) return ((key & 3) << 2) | ((key >> 2) & 3);
+  else return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (the LDS DMA loads count there); LDS and export counters are not waited on.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// 16 bytes per lane from global memory straight into LDS (the DMA form of
+// global_load_dwordx4): lane i's bytes land at dst + 16 i, dst wave-uniform.
+__device__ __forceinline__ void lds_dma16(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+// Workgroup barrier for the LDS ring. Each wave has waited for its own DMA
+// loads before it arrives; the empty asm statements keep the compiler from
+// moving LDS accesses across the barrier.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 
 template <int D>
 __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
@@ -66,19 +116,24 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
     int64_t slots_per_head) {
   constexpr int NT = 64 * kAttnWaves;
-  constexpr int KB = kTileKeys / 32;  // 32-key blocks per stage
-  constexpr int KS = D / 16;          // MFMA steps over head_dim
-  constexpr int DB = D / 32;          // 32-wide output column blocks
-  constexpr int PS = kTileKeys / 16;  // MFMA steps over the stage's keys
-  constexpr int KROW = D + 8;         // K stage row: 16-byte pad
-  constexpr int VROW = kTileKeys + 4; // V^T stage row: 8-byte pad
-  constexpr int KCH = kTileKeys * D / 8 / NT;       // 16-byte K chunks per thread
-  constexpr int VUNITS = (kTileKeys / 4) * (D / 8); // (4 keys x 8 dims) V units
-  static_assert(KCH >= 1 && VUNITS <= NT, "staging does not tile");
-  __shared__ __attribute__((aligned(16))) bf16_t lds_k[kStages][kTileKeys][KROW];
-  __shared__ __attribute__((aligned(16))) bf16_t lds_v[kStages][D][VROW];
+  constexpr int KB = kTileKeys / 32;   // 32-key blocks per stage
+  constexpr int KS = D / 16;           // MFMA steps over head_dim
+  constexpr int DB = D / 32;           // 32-wide output column blocks
+  constexpr int PS = kTileKeys / 16;   // MFMA steps over the stage's keys
+  constexpr int ROWB = 2 * D;          // bytes of one history row of one head
+  constexpr int CR = D / 8;            // 16-byte chunks per row
+  constexpr int STAGE = kTileKeys * ROWB;             // bytes of one K (or V) stage
+  constexpr int KPI = 1024 / ROWB;                    // rows per wave-wide DMA load
+  constexpr int NI = kTileKeys / (KPI * kAttnWaves);  // DMA loads per wave, operand, stage
+  constexpr int NL = 2 * NI;                          // DMA loads per thread per stage
+  static_assert(NI >= 1 && kTileKeys % (KPI * kAttnWaves) == 0, "staging does not tile");
+  static_assert(NT == 512 && CR * 16 == ROWB, "layout");
+  static_assert(kStages * STAGE <= 65536, "LDS offsets must fit the 16-bit immediate");
+  __shared__ __attribute__((aligned(1024))) char lds[2 * kStages * STAGE];  // K ring, V ring
+  ROCS_LDS char* const lds3 = (ROCS_LDS char*)lds;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
   const uint32_t work = xcd_remap(blockIdx.x, gridDim.x);
   const int h = (int)(work / (uint64_t)slots_per_head);
@@ -112,70 +167,61 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
   for (int ks = 0; ks < KS; ++ks)
     qf[ks] = *reinterpret_cast<const bf16x8*>(qh + qrow * qs + 16 * ks + 8 * hh);
 
-  // K/V staging. K: chunk c -> key c / (D/8), dims (c % (D/8)) * 8.
-  // V: unit u -> keys 4 (u % 16) .. +3, dims (u / 16) * 8 .. +7, written
-  // transposed as eight 4-key rows. Each thread keeps pointers to its rows of
-  // stage 0 and adds the stage offset; only the last stage clamps key
-  // indices to L - 1.
-  const bf16_t* kh = k + kv0 * kv_stride + (int64_t)h * D;
-  const bf16_t* vh = v + kv0 * kv_stride + (int64_t)h * D;
-  const bool has_v = tid < VUNITS;
-  const int vkg = tid % 16, vdc = (tid / 16) * 8;
-  const bf16_t* kp[KCH];
-  int kkey[KCH];
+  // DMA staging. Load i of wave w fills LDS rows KPI (NI w + i) .. +KPI-1 of
+  // the stage, 16 bytes per lane in lane order: lane -> row KPI (NI w + i) +
+  // lane / CR, chunk position lane % CR, so the lane fetches chunk
+  // (lane % CR) ^ kv_swizzle(row) of that history row.
+  const char* kbase = reinterpret_cast<const char*>(k + kv0 * kv_stride + (int64_t)h * D);
+  const char* vbase = reinterpret_cast<const char*>(v + kv0 * kv_stride + (int64_t)h * D);
+  const int64_t rowstride = kv_stride * 2;                // bytes
+  int skey[NI];
+  uint32_t schunk[NI], soff[NI];
 #pragma unroll
-  for (int i = 0; i < KCH; ++i) {
-    const int c = tid + NT * i;
-    kkey[i] = c / (D / 8);
-    kp[i] = kh + (int64_t)kkey[i] * kv_stride + (c % (D / 8)) * 8;
+  for (int i = 0; i < NI; ++i) {
+    skey[i] = KPI * (NI * wave + i) + lane / CR;
+    schunk[i] = 16u * (uint32_t)((lane % CR) ^ kv_swizzle<D>(skey[i]));
+    soff[i] = (uint32_t)(skey[i] * rowstride) + schunk[i];
   }
-  const bf16_t* vp = vh + (int64_t)(4 * vkg) * kv_stride + vdc;
-  u32x4 rk[KCH], rv[4];
-  auto load_kv = [&](int base) {
-    const int64_t off = (int64_t)base * kv_stride;
+  auto issue = [&](int t) {
+    const int base = t * kTileKeys;
+    char* kdst = lds + (t % kStages) * STAGE;
+    char* vdst = kdst + kStages * STAGE;
     if (base + kTileKeys <= L) {
+      const char* ks = kbase + base * rowstride;
+      const char* vs = vbase + base * rowstride;
 #pragma unroll
-      for (int i = 0; i < KCH; ++i) rk[i] = *reinterpret_cast<const u32x4*>(kp[i] + off);
-      if (has_v) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          rv[e] = *reinterpret_cast<const u32x4*>(vp + off + (int64_t)e * kv_stride);
+      for (int i = 0; i < NI; ++i) {
+        lds_dma16(ks + soff[i], kdst + KPI * (NI * wave + i) * ROWB);
+        lds_dma16(vs + soff[i], vdst + KPI * (NI * wave + i) * ROWB);
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < KCH; ++i) {
-        const int key = min(base + kkey[i], L - 1) - kkey[i];
-        rk[i] = *reinterpret_cast<const u32x4*>(kp[i] + (int64_t)key * kv_stride);
-      }
-      if (has_v) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = min(base + 4 * vkg + e, L - 1) - 4 * vkg;
-          rv[e] = *reinterpret_cast<const u32x4*>(vp + (int64_t)key * kv_stride);
-        }
-      }
-    }
-  };
-  auto store_kv = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < KCH; ++i) {
-      const int c = tid + NT * i;
-      *reinterpret_cast<u32x4*>(&lds_k[buf][kkey[i]][(c % (D / 8)) * 8]) = rk[i];
-    }
-    if (has_v) {
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // dims vdc + 2w (low halves of the four keys) and vdc + 2w + 1 (high halves)
-        const u32x2 lo = {__builtin_amdgcn_perm(rv[1][w], rv[0][w], 0x05040100u),
-                          __builtin_amdgcn_perm(rv[3][w], rv[2][w], 0x05040100u)};
-        const u32x2 hi = {__builtin_amdgcn_perm(rv[1][w], rv[0][w], 0x07060302u),
-                          __builtin_amdgcn_perm(rv[3][w], rv[2][w], 0x07060302u)};
-        *reinterpret_cast<u32x2*>(&lds_v[buf][vdc + 2 * w][4 * vkg]) = lo;
-        *reinterpret_cast<u32x2*>(&lds_v[buf][vdc + 2 * w + 1][4 * vkg]) = hi;
+      for (int i = 0; i < NI; ++i) {
+        const int64_t o = (int64_t)min(base + skey[i], L - 1) * rowstride + schunk[i];
+        lds_dma16(kbase + o, kdst + KPI * (NI * wave + i) * ROWB);
+        lds_dma16(vbase + o, vdst + KPI * (NI * wave + i) * ROWB);
       }
     }
   };
 
+  // LDS fragment addresses (bytes, stage 0). K: row 32 kb + l32, chunk
+  // 2 ks + hh; the swizzle turns the ks step into an XOR with 32 ks.
+  const uint32_t ka0 = (uint32_t)(l32 * ROWB + 16 * (hh ^ kv_swizzle<D>(l32)));
+  // V, transposing read r of step ps: 16-lane group g = lane / 16 reads rows
+  // 16 ps + 4 (g / 2) + 8 r + (lane % 16) / 4, dims 32 db + 16 (g % 2) +
+  // 4 (lane % 4) .. +3; the db step is an XOR with 64 db.
+  uint32_t va0[2];
+#pragma unroll
+  for (int rr = 0; rr < 2; ++rr) {
+    const int g = lane >> 4, jl = lane & 15;
+    const int key = 4 * (g >> 1) + 8 * rr + (jl >> 2);
+    const int chunk0 = 2 * (g & 1) + ((jl & 3) >> 1);
+    va0[rr] = (uint32_t)(kStages * STAGE + key * ROWB + 16 * (chunk0 ^ kv_swizzle<D>(key)) +
+                         8 * (jl & 1));
+  }
+
+  const int ntiles = (L + kTileKeys - 1) / kTileKeys;
+  const int last_valid = L - (ntiles - 1) * kTileKeys;    // keys in the last stage
   float m_run = -INFINITY, l_part = 0.f;
   f32x16 oacc[DB];
 #pragma unroll
@@ -194,7 +240,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
     for (int ks = 0; ks < KS; ++ks) {
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(&lds_k[buf][32 * kb + l32][16 * ks + 8 * hh]);
+        const bf16x8 a = *reinterpret_cast<const ROCS_LDS bf16x8*>(
+            lds3 + ((ka0 ^ (32u * ks)) + buf * STAGE + kb * 32 * ROWB));
         sacc[kb] = mfma32(a, qf[ks], sacc[kb]);
       }
       // Keep at most two steps of K fragments in flight (register budget for
@@ -203,8 +250,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
     }
   };
 
-  // Softmax, first half: mask (last stage only), row max and the lazy
-  // rescale of the running state.
+  // Row max of one stage (masking the keys past the history's end in the
+  // last stage) and the move of the running max: only when the stage max
+  // exceeds it by more than 2^kLazyRescale (always on the first stage).
   auto row_max = [&](f32x16 (&sacc)[KB], auto masked, int valid) {
     if constexpr (decltype(masked)::value) {
 #pragma unroll
@@ -231,69 +279,112 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
     }
   };
 
-  // Softmax, second half: probabilities and the PV product against the V^T
-  // in LDS buffer `buf`.
-  auto exp_pv = [&](int buf, f32x16 (&sacc)[KB]) {
-    // Probabilities (bf16) as B fragments of the PV product. MFMA step ps
-    // covers keys 16 ps + 4 hh + {0..3} and 16 ps + 8 + 4 hh + {0..3}:
-    // elements 8 (ps % 2) .. +7 of sacc[ps / 2].
+  // Weights of MFMA step ps as packed bf16 B fragments: step ps covers keys
+  // 16 ps + 4 hh + {0..3} and 16 ps + 8 + 4 hh + {0..3}, elements
+  // 8 (ps % 2) .. +7 of sacc[ps / 2]. Each packed pair is a scalar of its
+  // own: the row-sum dot2 must not read its operand out of a vector register
+  // tuple (the gfx950 code generator has been seen to feed the same tuple
+  // element to every dot2 in that form). `lst` sums the bf16-rounded weights
+  // the PV product uses.
+  auto exp_block = [&](const f32x16 (&sacc)[KB], int ps, uint32_t (&pk)[4], float& lst) {
     const bf16x2 ones = {(bf16_t)1.0f, (bf16_t)1.0f};
 #pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float s0 = sacc[ps / 2][8 * (ps % 2) + 2 * w];
+      const float s1 = sacc[ps / 2][8 * (ps % 2) + 2 * w + 1];
+      pk[w] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(s0, scale_log2, -m_run)),
+                          __builtin_amdgcn_exp2f(fmaf(s1, scale_log2, -m_run)));
+      lst = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[w]), ones, lst, false);
+    }
+  };
+  // O^T += V^T P^T for step ps: the A lane holds V^T[32 db + l32][the same
+  // 8 keys], read transposed out of the row-major V stage.
+  auto pv_block = [&](int buf, int ps, const uint32_t (&pk)[4]) {
+    const bf16x8 pf = as_bf16x8(u32x4{pk[0], pk[1], pk[2], pk[3]});
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint32_t off = buf * STAGE + ps * 16 * ROWB;
+      const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (ROCS_LDS i16x4*)(lds3 + ((va0[0] ^ (64u * db)) + off))));
+      const u32x2 hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (ROCS_LDS i16x4*)(lds3 + ((va0[1] ^ (64u * db)) + off))));
+      oacc[db] = mfma32(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pf, oacc[db]);
+    }
+  };
+  // One stage of the software pipeline: the scores of the next stage (LDS
+  // buffer nbuf) on the matrix cores, interleaved step by step with the
+  // weights of this stage on the VALU; then this stage's PV product. The
+  // weights use the running max as it stands; their per-lane sum bounds each
+  // of them, so a stage whose sum stays below 2^kLazyRescale needs no max at
+  // all. Otherwise (first stage, a jump of the scores, inf or NaN) the stage
+  // takes the row max and recomputes its weights.
+  auto stage = [&](int nbuf, f32x16 (&snext)[KB], int buf, f32x16 (&sacc)[KB]) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) snext[kb][e] = 0.f;
+    uint32_t pk[PS][4];
+    float lst = 0.f;
+#pragma unroll
     for (int ps = 0; ps < PS; ++ps) {
-      // Each packed pair is a scalar of its own: the row-sum dot2 must not
-      // read its operand out of a vector register tuple (the gfx950 code
-      // generator has been seen to feed the same tuple element to every dot2
-      // in that form).
-      uint32_t pk[4];
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float s0 = sacc[ps / 2][8 * (ps % 2) + 2 * w];
-        const float s1 = sacc[ps / 2][8 * (ps % 2) + 2 * w + 1];
-        pk[w] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(s0, scale_log2, -m_run)),
-                            __builtin_amdgcn_exp2f(fmaf(s1, scale_log2, -m_run)));
-        l_part = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk[w]), ones, l_part,
-                                                 false);
-      }
-      const bf16x8 pf = as_bf16x8(u32x4{pk[0], pk[1], pk[2], pk[3]});
-      // O^T += V^T P^T: A lane holds V^T[32 db + l32][the same 8 keys].
+      for (int ks = (KS / PS) * ps; ks < (KS / PS) * (ps + 1); ++ks)
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(&lds_v[buf][32 * db + l32][16 * ps + 4 * hh]);
-        const u32x2 hi =
-            *reinterpret_cast<const u32x2*>(&lds_v[buf][32 * db + l32][16 * ps + 8 + 4 * hh]);
-        oacc[db] = mfma32(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pf, oacc[db]);
-      }
+        for (int kb = 0; kb < KB; ++kb) {
+          const bf16x8 a = *reinterpret_cast<const ROCS_LDS bf16x8*>(
+              lds3 + ((ka0 ^ (32u * ks)) + nbuf * STAGE + kb * 32 * ROWB));
+          snext[kb] = mfma32(a, qf[ks], snext[kb]);
+        }
+      exp_block(sacc, ps, pk[ps], lst);
       __builtin_amdgcn_sched_barrier(0);
     }
+    if (__builtin_expect(__ballot(!(lst <= kWeightBound)) != 0, 0)) {
+      row_max(sacc, std::false_type(), kTileKeys);
+      lst = 0.f;
+#pragma unroll
+      for (int ps = 0; ps < PS; ++ps) exp_block(sacc, ps, pk[ps], lst);
+    }
+    l_part += lst;
+#pragma unroll
+    for (int ps = 0; ps < PS; ++ps) {
+      pv_block(buf, ps, pk[ps]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // The last (possibly ragged) stage: masked row max, weights, PV.
+  auto last_stage = [&](int buf, f32x16 (&sacc)[KB]) {
+    row_max(sacc, std::true_type(), last_valid);
+    uint32_t pk[PS][4];
+    float lst = 0.f;
+#pragma unroll
+    for (int ps = 0; ps < PS; ++ps) exp_block(sacc, ps, pk[ps], lst);
+    l_part += lst;
+#pragma unroll
+    for (int ps = 0; ps < PS; ++ps) pv_block(buf, ps, pk[ps]);
   };
 
   // Software pipeline over stages: while the matrix cores compute the scores
   // of stage t + 1, the VALU runs the softmax of stage t, then stage t's PV
-  // product follows. K/V live in a 3-deep LDS ring (stages t, t + 1 and the
-  // one being filled for t + 2), so one barrier per stage suffices.
-  const int ntiles = (L + kTileKeys - 1) / kTileKeys;
-  const int last_valid = L - (ntiles - 1) * kTileKeys;    // keys in the last stage
-  load_kv(0);
-  store_kv(0);
-  if (ntiles > 1) {
-    load_kv(kTileKeys);
-    store_kv(1);
+  // product follows. Stage t + 3 is being loaded meanwhile; one barrier per
+  // stage hands the ring slots around.
+  issue(0);
+  if (ntiles > 1) issue(1);
+  if (ntiles > 2) {
+    issue(2);
+    wait_vmcnt<NL>();                                     // stages 0 and 1 resident
+  } else {
+    wait_vmcnt<0>();
   }
-  __syncthreads();
-  // One pipelined step: finish the softmax bookkeeping of stage kt (scores
-  // in s_cur), start the scores of stage kt + 1 into s_next on the matrix
-  // cores, and let the VALU exponentiate stage kt meanwhile, then its PV.
+  ring_barrier();
   f32x16 s_a[KB], s_b[KB];
   auto step = [&](int kt, f32x16 (&s_cur)[KB], f32x16 (&s_next)[KB]) {
-    const bool fill = kt + 2 < ntiles;
-    if (fill) load_kv((kt + 2) * kTileKeys);
+    const bool fill = kt + 3 < ntiles;
+    if (fill) issue(kt + 3);
     if (active) {
-      row_max(s_cur, std::false_type(), kTileKeys);
-      qk((kt + 1) % kStages, s_next);
-      exp_pv(kt % kStages, s_cur);
+      stage((kt + 1) % kStages, s_next, kt % kStages, s_cur);
     }
-    if (fill) store_kv((kt + 2) % kStages);
-    __syncthreads();
+    if (fill) wait_vmcnt<NL>(); else wait_vmcnt<0>();     // stage kt + 2 resident
+    ring_barrier();
   };
   if (active) qk(0, s_a);
   int kt = 0;
@@ -303,13 +394,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
   }
   if (kt + 1 < ntiles) {
     step(kt, s_a, s_b);
-    if (active) {
-      row_max(s_b, std::true_type(), last_valid);
-      exp_pv((ntiles - 1) % kStages, s_b);
-    }
+    if (active) last_stage((ntiles - 1) % kStages, s_b);
   } else if (active) {
-    row_max(s_a, std::true_type(), last_valid);
-    exp_pv((ntiles - 1) % kStages, s_a);
+    last_stage((ntiles - 1) % kStages, s_a);
   }
 
   if (!active) return;

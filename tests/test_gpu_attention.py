@@ -50,6 +50,23 @@ def test_peaked_scores_exercise_rescaling(gpu_lib):
     assert_close(_attn(case, scale=0.01), _want(case, scale=0.01), "explicit scale")
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_running_max_jumps_past_the_weight_bound(gpu_lib, head_dim):
+    # Scores far apart in the exp2 domain (more than 64 between stages), so
+    # stages after the first must move the running max and redo their weights.
+    case = wl.attention_case([300, 70], [700, 129], 2, head_dim, seed=11)
+    assert_close(_attn(case, scale=4.0), _want(case, scale=4.0), f"scale 4 d{head_dim}")
+    # A ramp: score of history row j is 64 (j mod 256) / 8 / sqrt(d), rising
+    # by more than 64 (exp2 domain) from one 64-key stage to the next.
+    q = np.zeros_like(case.q)
+    q[..., 0] = 64.0
+    k = np.zeros_like(case.k)
+    local = np.concatenate([np.arange(n) for n in np.diff(case.kv_offsets)])
+    k[:, :, 0] = ((local % 256) / 8.0)[:, None]
+    ramp = type(case)(**{**vars(case), "q": q, "k": k})
+    assert_close(_attn(ramp), _want(ramp), f"ramp d{head_dim}")
+
+
 def test_single_key_is_exact(gpu_lib):
     # L = 1: the one weight is exactly 1, so the output is that value row.
     case = wl.attention_case([37, 300], [1, 1], 2, 128, seed=10, q_std=4.0)
