@@ -73,9 +73,6 @@ constexpr float kWeightBound = 0x1p64f;
 constexpr int kAttnWaves = 8;
 constexpr int kStages = 4;       // K/V ring depth in LDS (loads run two stages ahead)
 
-#define ROCS_LDS __attribute__((address_space(3)))
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-
 // 16-byte chunk c of history row `key` (D bf16 = 2D bytes) sits at chunk
 // position c ^ kv_swizzle(key) of its LDS row. Conflict-free for both read
 // patterns: 16 consecutive rows at one chunk (K fragments) and 4 consecutive
@@ -84,29 +81,6 @@ template <int D>
 __device__ __forceinline__ int kv_swizzle(int key) {
   if constexpr (D == 128) return ((key & 3) << 2) | ((key >> 2) & 3);
   else return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
-}
-
-// Wait until at most N vector-memory operations of this wave are in flight
-// (the LDS DMA loads count there); LDS and export counters are not waited on.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt field");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// 16 bytes per lane from global memory straight into LDS (the DMA form of
-// global_load_dwordx4): lane i's bytes land at dst + 16 i, dst wave-uniform.
-__device__ __forceinline__ void lds_dma16(const void* src, void* dst) {
-  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
-}
-
-// Workgroup barrier for the LDS ring. Each wave has waited for its own DMA
-// loads before it arrives; the empty asm statements keep the compiler from
-// moving LDS accesses across the barrier.
-__device__ __forceinline__ void ring_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 template <int D>
@@ -182,17 +156,18 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
     schunk[i] = 16u * (uint32_t)((lane % CR) ^ kv_swizzle<D>(skey[i]));
     soff[i] = (uint32_t)(skey[i] * rowstride) + schunk[i];
   }
+  const uint32_t lds_base = lds_addr(lds);
   auto issue = [&](int t) {
     const int base = t * kTileKeys;
-    char* kdst = lds + (t % kStages) * STAGE;
-    char* vdst = kdst + kStages * STAGE;
+    const uint32_t kdst = lds_base + (uint32_t)((t % kStages) * STAGE);
+    const uint32_t vdst = kdst + kStages * STAGE;
     if (base + kTileKeys <= L) {
       const char* ks = kbase + base * rowstride;
       const char* vs = vbase + base * rowstride;
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
-        lds_dma16(ks + soff[i], kdst + KPI * (NI * wave + i) * ROWB);
-        lds_dma16(vs + soff[i], vdst + KPI * (NI * wave + i) * ROWB);
+        lds_dma16_sv(ks, soff[i], kdst + KPI * (NI * wave + i) * ROWB);
+        lds_dma16_sv(vs, soff[i], vdst + KPI * (NI * wave + i) * ROWB);
       }
     } else {
 #pragma unroll
@@ -369,12 +344,11 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
   // stage hands the ring slots around.
   issue(0);
   if (ntiles > 1) issue(1);
-  if (ntiles > 2) {
-    issue(2);
-    wait_vmcnt<NL>();                                     // stages 0 and 1 resident
-  } else {
-    wait_vmcnt<0>();
-  }
+  if (ntiles > 2) issue(2);
+  // Everything resident, the query fragments included: from here on the
+  // only vector-memory operations in flight are the ring's DMA loads, which
+  // the compiler does not track, so it adds no waits of its own in the loop.
+  wait_vmcnt<0>();
   ring_barrier();
   f32x16 s_a[KB], s_b[KB];
   auto step = [&](int kt, f32x16 (&s_cur)[KB], f32x16 (&s_next)[KB]) {

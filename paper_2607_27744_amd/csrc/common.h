@@ -136,4 +136,47 @@ __device__ __forceinline__ float sum_across_rows(float v) {
   return __builtin_bit_cast(float, (int)s32[0]) + __builtin_bit_cast(float, (int)s32[1]);
 }
 
+#define ROCS_LDS __attribute__((address_space(3)))
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (loads, stores and the LDS DMA loads all count there, and complete in
+// issue order); LDS and export counters are not waited on.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// 16 bytes per lane from global memory straight into LDS (the DMA form of
+// global_load_dwordx4): lane i's bytes land at dst + 16 i, dst wave-uniform.
+// Written as inline assembly on purpose: the compiler does not see an LDS
+// write, so it adds no wait for these loads before unrelated LDS reads (its
+// alias check would otherwise wait for every DMA load in flight before each
+// LDS read of the ring). The caller orders LDS reads after the loads with
+// wait_vmcnt and a barrier. The compiler does not count these loads either,
+// which only makes its own vector-memory waits stricter.
+// LDS byte address of a __shared__ object (wave-uniform).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const ROCS_LDS void*)p);
+}
+// `dst` is an LDS byte address, wave-uniform.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t dst) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" :: "v"(src), "s"(dst) : "m0");
+}
+// Same with a wave-uniform base address and a 32-bit per-lane byte offset.
+__device__ __forceinline__ void lds_dma16_sv(const void* sbase, uint32_t voff, uint32_t dst) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(sbase), "s"(dst) : "m0");
+}
+
+// Workgroup barrier for the LDS ring. Each wave has waited for its own DMA
+// loads before it arrives; the empty asm statements keep the compiler from
+// moving LDS accesses across the barrier.
+__device__ __forceinline__ void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 }  // namespace rocs

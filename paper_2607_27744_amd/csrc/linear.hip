@@ -29,16 +29,17 @@ __global__ __launch_bounds__(256) void request_ids_kernel(const int32_t* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Request-side GEMM, bf16 in, fp32 Z out. One workgroup per 16 x 16 tile of
-// Z; its four waves split K in 32-wide steps (operands straight from global
-// memory into MFMA registers, each lane's 8 consecutive k are one 16-byte
-// load) and reduce through LDS in a fixed order. Workgroups past the Z tiles
-// expand the index map.
+// Request-side GEMM, bf16 in, fp32 out: the request table Zb = X^R W_CR^T + b
+// (the bias is folded in here, once per request). One workgroup per 16 x 16
+// tile of Zb; its four waves split K in 32-wide steps (operands straight from
+// global memory into MFMA registers, each lane's 8 consecutive k are one
+// 16-byte load) and reduce through LDS in a fixed order. Workgroups past the
+// Zb tiles expand the index map when the candidate GEMM needs it.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void request_gemm_bf16(
-    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, float* __restrict__ z,
-    const int32_t* __restrict__ off, int32_t* __restrict__ ids, int R, int64_t N, int K, int D,
-    int tiles_d, int z_blocks) {
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, const float* __restrict__ bias,
+    float* __restrict__ z, const int32_t* __restrict__ off, int32_t* __restrict__ ids, int R,
+    int64_t N, int K, int D, int tiles_d, int z_blocks) {
   const int tid = threadIdx.x;
   if ((int)blockIdx.x >= z_blocks) {
     const int64_t n = (int64_t)(blockIdx.x - z_blocks) * 256 + tid;
@@ -63,9 +64,12 @@ __global__ __launch_bounds__(256) void request_gemm_bf16(
   red[wave][lane] = acc;
   __syncthreads();
   if (wave == 0) {
-    const f32x4 s = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+    f32x4 s = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
     const int d = d0 + (lane >> 4) * 4;
-    if (rok && d < D) *reinterpret_cast<f32x4*>(z + (int64_t)(r0 + row) * D + d) = s;
+    if (rok && d < D) {
+      if (bias != nullptr) s += *reinterpret_cast<const f32x4*>(bias + d);
+      *reinterpret_cast<f32x4*>(z + (int64_t)(r0 + row) * D + d) = s;
+    }
   }
 }
 
@@ -223,6 +227,379 @@ void ikbo_gemm_bf16(
 }
 
 // ---------------------------------------------------------------------------
+// Streaming candidate GEMM (bf16, K a multiple of 64), the main path.
+//
+// Persistent workgroups, one per CU, walk the 256 (features) x 256
+// (candidates) output tiles with a stride of the grid; four waves, one per
+// SIMD, each own a 128 x 128 quarter (16 MFMA 32x32 accumulators, 256 of the
+// wave's 512 registers). K arrives in 64-wide slabs (128-byte row segments:
+// whole cache lines, which the L2 serves at twice the rate of half lines)
+// through LDS rings filled by LDS DMA loads, as one stream across tile
+// boundaries: the weight slab (L2-resident) one slab ahead of use in a
+// 2-deep ring, the candidate slab (from HBM, longer latency) two slabs ahead
+// in a 3-deep ring; together exactly the 160 KiB of LDS. The loads are
+// issued one at a time between the MFMAs. The 16-byte chunks of each slab
+// row are XOR-swizzled by (row / 2) % 8, which puts the 16 rows read by each
+// quarter-wave on distinct banks; fragments are read one k-step ahead.
+//
+// IKBO tiling (Section 4.2.1): with a request term, tiles never straddle two
+// requests: request r owns tile slots r + floor(off[r] / 256) ... (the last
+// one partial), so the whole tile shares one row of the request table
+// Zb = X^R W_CR^T + b, added in the epilogue (the broadcast add fused into
+// the GEMM). Without a request term the tiles cover the candidate rows
+// contiguously and Zb is the bias (or absent).
+//
+// Epilogue: Zb, activation on packed bf16, then the two wave halves swap
+// 8-byte pieces so every lane holds 8 consecutive features: 16-byte stores,
+// which drain while the next tile computes.
+//
+// Rows past the tile's end are clamped loads whose results are not stored.
+// ---------------------------------------------------------------------------
+constexpr int kStreamBM = 256, kStreamBN = 256, kStreamBK = 64;
+
+// ReLU of two packed bf16 values: as 16-bit integers the negative values
+// (sign bit set) are exactly those below zero, so a packed integer max with
+// zero clamps them (and -0) to +0. Written as the one instruction: the
+// compiler's own lowering of a packed max on a bit-cast pair has been seen
+// to drop the second word of the pair.
+__device__ __forceinline__ uint32_t relu_bf16x2(uint32_t p) {
+  uint32_t r;
+  asm("v_pk_max_i16 %0, %1, 0" : "=v"(r) : "v"(p));
+  return r;
+}
+
+struct StreamTile {
+  int slot;       // tile slot (candidate block)
+  int mb;         // feature block
+  int r;          // request of the slot (0 without a request term)
+  int64_t n0;     // first candidate row
+  int rows;       // candidate rows in the tile
+  int m0;         // first output feature
+};
+
+// Tiles are numbered slot * tiles_m + mb and a workgroup takes every
+// grid-th one; the step is passed split into (slot, mb) parts so that no
+// division runs on the device.
+struct StreamStep {
+  int slots, mbs;                  // grid = slots * tiles_m + mbs, mbs < tiles_m
+};
+
+__device__ __forceinline__ void stream_next(StreamTile& c, StreamStep st, int tiles_m) {
+  c.slot += st.slots;
+  c.mb += st.mbs;
+  if (c.mb >= tiles_m) {
+    c.mb -= tiles_m;
+    ++c.slot;
+  }
+}
+
+// Move `c` forward (in grid steps) to the first tile that holds candidate
+// rows; false when the slots are exhausted. All values are wave-uniform.
+template <typename OffPtr>
+__device__ __forceinline__ bool stream_seek(StreamTile& c, StreamStep st, int n_slots,
+                                            int tiles_m, OffPtr off, int R, int64_t N) {
+  for (; c.slot < n_slots; stream_next(c, st, tiles_m)) {
+    c.m0 = c.mb * kStreamBM;
+    if (off != nullptr) {
+      auto base_of = [&](int r) { return (int64_t)r + off[r] / kStreamBN; };   // tile slots
+      while (c.r + 1 < R && base_of(c.r + 1) <= c.slot) ++c.r;
+      const int64_t end = off[c.r + 1];
+      c.n0 = (int64_t)off[c.r] + (c.slot - base_of(c.r)) * kStreamBN;
+      if (c.n0 < end) {
+        c.rows = (int)(end - c.n0 < kStreamBN ? end - c.n0 : kStreamBN);
+        return true;
+      }
+    } else {
+      c.n0 = (int64_t)c.slot * kStreamBN;
+      c.rows = (int)(N - c.n0 < kStreamBN ? N - c.n0 : kStreamBN);
+      return true;
+    }
+  }
+  return false;
+}
+
+template <bool HAS_ZB, bool RELU>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
+                      const float* __restrict__ zb, const int32_t* __restrict__ off_g,
+                      bf16_t* __restrict__ out, int R, int64_t N, int K, int D, int tiles_m,
+                      int n_slots, StreamStep step_g) {
+  constexpr int BM = kStreamBM, BN = kStreamBN, BK = kStreamBK;
+  constexpr int NSA = 2, NSB = 3;                // ring depths: weights, candidates
+  constexpr int ROWB = BK * 2;                   // bytes of one slab row (128)
+  constexpr int RPI = 1024 / ROWB;               // slab rows per wave-wide DMA load (8)
+  constexpr int NI = BM / RPI / 4;               // DMA loads per wave and operand (8)
+  constexpr int SLAB = BM * ROWB;                // bytes of one operand slab (32 KiB)
+  constexpr int BBASE = NSA * SLAB;              // candidate ring after the weight ring
+  static_assert(BM == BN && NI * RPI * 4 == BM && ROWB == 128, "tiling");
+  static_assert((NSA + NSB) * SLAB <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) char lds[(NSA + NSB) * SLAB];
+  ROCS_LDS char* const lds3 = (ROCS_LDS char*)lds;
+  // The offsets are read-only for the kernel's lifetime: read them through
+  // the constant address space (scalar loads).
+  const __attribute__((address_space(4))) int32_t* off =
+      (const __attribute__((address_space(4))) int32_t*)off_g;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, hh = lane >> 5, h4 = 4 * hh;
+  const int wm0 = (wave & 1) * 128, wn0 = (wave >> 1) * 128;
+  const int nk = K / BK;
+  const int rowb = K * 2;
+  const int first = (int)xcd_remap(blockIdx.x, gridDim.x);
+  const uint32_t lbase = lds_addr(lds);
+
+  // DMA lane map: load i of this wave fills slab rows RPI (NI wave + i) +
+  // lane / 8, chunk position lane % 8, with chunk (lane % 8) ^ ((row / 2) % 8).
+  // Rows past the operand's valid rows are clamped to the last valid one.
+  const int drow0 = RPI * NI * wave + (lane >> 3);
+  auto dma_piece = [&](const char* src, int rowlim, uint32_t dst, int i) __attribute__((always_inline)) {
+    const int row = drow0 + RPI * i;
+    const uint32_t chunk = 16u * (uint32_t)((lane & 7) ^ ((row >> 1) & 7));
+    lds_dma16_sv(src, (uint32_t)(min(row, rowlim) * rowb) + chunk,
+                 dst + (uint32_t)(RPI * (NI * wave + i) * ROWB));
+  };
+
+  // The issue cursor walks the slab sequence two slabs ahead of compute and
+  // plans the candidate slab; the weight slab of the same position follows
+  // one slab later (weights sit in L2, candidates come from HBM).
+  StreamTile ic{first / tiles_m, first % tiles_m, 0, 0, 0, 0};
+  bool ic_live = stream_seek(ic, step_g, n_slots, tiles_m, off, R, N);
+  int ic_s = 0;
+  int buf_b = 0, buf_a = 0;              // ring slots of the next loads
+  const char* a_next_src = nullptr;      // weight slab queued behind the candidates
+  int a_next_lim = 0;
+  bool a_queued = false;
+  // Loads planned for the current slab: weights of slab g + 1, candidates
+  // of slab g + 2. They are issued one at a time between the MFMAs.
+  const char* pa_src = nullptr;
+  int pa_lim = 0;
+  uint32_t pa_dst = 0;
+  bool pa_on = false;
+  const char* pb_src = nullptr;
+  int pb_lim = 0;
+  uint32_t pb_dst = 0;
+  bool pb_on = false;
+  auto plan_b = [&]() __attribute__((always_inline)) {
+    const int kb = ic_s * ROWB;
+    pb_src = reinterpret_cast<const char*>(x + ic.n0 * K) + kb;
+    pb_lim = ic.rows - 1;
+    pb_dst = lbase + (uint32_t)(BBASE + buf_b * SLAB);
+    pb_on = true;
+    buf_b = buf_b == NSB - 1 ? 0 : buf_b + 1;
+    a_next_src = reinterpret_cast<const char*>(w + (int64_t)ic.m0 * K) + kb;
+    a_next_lim = D - 1 - ic.m0;
+    a_queued = true;
+    if (++ic_s == nk) {
+      ic_s = 0;
+      stream_next(ic, step_g, tiles_m);
+      ic_live = stream_seek(ic, step_g, n_slots, tiles_m, off, R, N);
+    }
+  };
+  auto plan_a = [&]() __attribute__((always_inline)) {
+    pa_src = a_next_src;
+    pa_lim = a_next_lim;
+    pa_dst = lbase + (uint32_t)(buf_a * SLAB);
+    pa_on = true;
+    buf_a ^= 1;
+    a_queued = false;
+  };
+  // Piece p of the planned loads: weights 0..7, candidates 8..15.
+  auto dma_plan_piece = [&](int p) __attribute__((always_inline)) {
+    if (p < NI) {
+      if (pa_on) dma_piece(pa_src, pa_lim, pa_dst, p);
+    } else {
+      if (pb_on) dma_piece(pb_src, pb_lim, pb_dst, p - NI);
+    }
+  };
+
+  // Fragment addresses within an operand slab: row 32 f + l32 of the wave's
+  // quarter, chunk 2 ks + hh; the swizzle turns the ks step into XOR 32 ks.
+  const uint32_t fa0 = (uint32_t)(l32 * ROWB + 16 * (hh ^ ((l32 >> 1) & 7)));
+  f32x16 acc[4][4];
+  int cbuf_a = 0, cbuf_b = 0;            // ring slots of the slab being computed
+  auto compute = [&](auto first_slab) __attribute__((always_inline)) {
+    const uint32_t sa = (uint32_t)(cbuf_a * SLAB) + wm0 * ROWB;
+    const uint32_t sb = (uint32_t)(BBASE + cbuf_b * SLAB) + wn0 * ROWB;
+    // Fragments double-buffered across k-steps: the reads of step ks + 1 are
+    // in flight while the MFMAs of step ks run.
+    bf16x8 af[2][4], bfr[2][4];
+    auto load_frags = [&](int ks, int slot) __attribute__((always_inline)) {
+#pragma unroll
+      for (int f = 0; f < 4; ++f) {
+        af[slot][f] = *reinterpret_cast<const ROCS_LDS bf16x8*>(lds3 + sa + 32 * f * ROWB + (fa0 ^ (32u * ks)));
+        bfr[slot][f] = *reinterpret_cast<const ROCS_LDS bf16x8*>(lds3 + sb + 32 * f * ROWB + (fa0 ^ (32u * ks)));
+      }
+    };
+    load_frags(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < BK / 16; ++ks) {
+      const int cur = ks & 1;
+      if (ks + 1 < BK / 16) load_frags(ks + 1, cur ^ 1);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int fm = 0; fm < 4; ++fm) {
+#pragma unroll
+        for (int fn = 0; fn < 4; ++fn) {
+          if constexpr (decltype(first_slab)::value) {
+            if (ks == 0) {
+              const f32x16 zero = {};
+              acc[fm][fn] = mfma32(af[cur][fm], bfr[cur][fn], zero);
+              continue;
+            }
+          }
+          acc[fm][fn] = mfma32(af[cur][fm], bfr[cur][fn], acc[fm][fn]);
+        }
+        dma_plan_piece(4 * ks + fm);
+        // Keep MFMAs and loads in this order; ALU work may move.
+        __builtin_amdgcn_sched_barrier(0x0002 | 0x0004);
+      }
+    }
+  };
+
+  // Request row Zb[m0 + wm0 + 32 fm + 8 q + h4 .. +3] of the tile, loaded at
+  // the start of the tile's last slab and added in the epilogue.
+  f32x4 zv[4][4];
+  auto load_zb = [&](const StreamTile& c) __attribute__((always_inline)) {
+    if constexpr (HAS_ZB) {
+      const float* zr = zb + (int64_t)c.r * D;
+#pragma unroll
+      for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          zv[fm][q] = *reinterpret_cast<const f32x4*>(zr + min(c.m0 + wm0 + 32 * fm + 8 * q + h4, D - 4));
+    }
+  };
+
+  // Epilogue. Element 4 q + i of acc[fm][fn] is feature 32 fm + 8 q + h4 + i
+  // of candidate 32 fn + l32 (within the wave's quarter). For q = 2j, 2j + 1
+  // the lower half-wave keeps its q = 2j words and takes the upper half's,
+  // the upper half keeps q = 2j + 1 and takes the lower half's: then lane
+  // (l32, hh) holds features 32 fm + 16 j + 8 hh .. +7, one 16-byte store.
+  auto packed = [&](int fm, int fn, int q, uint32_t& lo, uint32_t& hi) __attribute__((always_inline)) {
+    const f32x16& a = acc[fm][fn];
+    float v0 = a[4 * q], v1 = a[4 * q + 1], v2 = a[4 * q + 2], v3 = a[4 * q + 3];
+    if constexpr (HAS_ZB) {
+      v0 += zv[fm][q][0];
+      v1 += zv[fm][q][1];
+      v2 += zv[fm][q][2];
+      v3 += zv[fm][q][3];
+    }
+    lo = pack_bf16x2(v0, v1);
+    hi = pack_bf16x2(v2, v3);
+    if constexpr (RELU) {
+      lo = relu_bf16x2(lo);
+      hi = relu_bf16x2(hi);
+    }
+  };
+  auto swapped = [&](int fm, int fn, int j) __attribute__((always_inline)) {
+    uint32_t e0, e1, o0, o1;                     // words of q = 2j and q = 2j + 1
+    packed(fm, fn, 2 * j, e0, e1);
+    packed(fm, fn, 2 * j + 1, o0, o1);
+    const auto s0 = __builtin_amdgcn_permlane32_swap(e0, o0, false, false);
+    const auto s1 = __builtin_amdgcn_permlane32_swap(e1, o1, false, false);
+    // Lower half: {own q = 2j, partner's q = 2j}; upper: {partner's q = 2j + 1, own}.
+    const uint32_t w0 = s0[0], w2 = s0[1], w1 = s1[0], w3 = s1[1];
+    return u32x4{w0, w1, w2, w3};
+  };
+  auto store_tile = [&](const StreamTile& c) __attribute__((always_inline)) {
+    const bool full = c.rows == BN && c.m0 + BM <= D;
+    if (full) {
+#pragma unroll
+      for (int fn = 0; fn < 4; ++fn) {
+        bf16_t* orow = out + (c.n0 + wn0 + 32 * fn + l32) * D + c.m0 + wm0 + 8 * hh;
+#pragma unroll
+        for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            *reinterpret_cast<u32x4*>(orow + 32 * fm + 16 * j) = swapped(fm, fn, j);
+      }
+      return;
+    }
+#pragma unroll
+    for (int fn = 0; fn < 4; ++fn) {
+      const int rr = wn0 + 32 * fn + l32;
+#pragma unroll
+      for (int fm = 0; fm < 4; ++fm)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          // The swap is wave-wide: every lane takes part, only valid ones
+          // store. D is a multiple of 4: a lane's 8 features are all valid,
+          // or only the first 4 (the row's last ones).
+          const u32x4 v = swapped(fm, fn, j);
+          const int d = c.m0 + wm0 + 32 * fm + 16 * j + 8 * hh;
+          if (rr < c.rows && d < D) {
+            bf16_t* p = out + (c.n0 + rr) * D + d;
+            if (d + 8 <= D) *reinterpret_cast<u32x4*>(p) = v;
+            else *reinterpret_cast<u32x2*>(p) = u32x2{v[0], v[1]};
+          }
+        }
+    }
+  };
+
+  // Prologue: candidates of slabs 0 and 1, weights of slab 0, all resident.
+  if (!ic_live) return;
+  StreamTile cc = ic;
+  plan_b();
+  plan_a();
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    dma_piece(pb_src, pb_lim, pb_dst, i);
+    dma_piece(pa_src, pa_lim, pa_dst, i);
+  }
+  if (ic_live) {
+    plan_b();
+#pragma unroll
+    for (int i = 0; i < NI; ++i) dma_piece(pb_src, pb_lim, pb_dst, i);
+  }
+  pa_on = pb_on = false;
+  wait_vmcnt<0>();
+  ring_barrier();
+
+  // One slab. Vector-memory operations retire in issue order. In an inner
+  // slab the candidate loads (slab g + 2) follow the weight loads (g + 1),
+  // so waiting until only those are in flight makes slab g + 1 resident. In
+  // the last slab of a tile the Zb loads go first, the candidates of slab
+  // g + 2 wait until after the epilogue, and the slab ends fully drained.
+  auto step = [&](auto first_slab, auto last_slab) __attribute__((always_inline)) {
+    constexpr bool kLast = decltype(last_slab)::value;
+    if constexpr (kLast) load_zb(cc);
+    const bool a_next = a_queued;
+    if (a_next) plan_a();
+    const bool b_next = ic_live;
+    if (!kLast && b_next) plan_b();
+    compute(first_slab);
+    pa_on = pb_on = false;
+    cbuf_a ^= 1;
+    cbuf_b = cbuf_b == NSB - 1 ? 0 : cbuf_b + 1;
+    if constexpr (kLast) {
+      wait_vmcnt<0>();
+      store_tile(cc);
+      if (b_next) {
+        plan_b();
+#pragma unroll
+        for (int i = 0; i < NI; ++i) dma_piece(pb_src, pb_lim, pb_dst, i);
+        pb_on = false;
+      }
+    } else {
+      if (b_next) wait_vmcnt<NI>(); else wait_vmcnt<0>();
+    }
+    if (a_next) ring_barrier();                  // a next slab exists
+  };
+  while (true) {
+    if (nk == 1) {
+      step(std::true_type(), std::true_type());
+    } else {
+      step(std::true_type(), std::false_type());
+      for (int s = 1; s < nk - 1; ++s) step(std::false_type(), std::false_type());
+      step(std::false_type(), std::true_type());
+    }
+    stream_next(cc, step_g, tiles_m);
+    if (!stream_seek(cc, step_g, n_slots, tiles_m, off, R, N)) break;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // General path: any dtype, any K / D, no alignment requirements.
 // ---------------------------------------------------------------------------
 template <typename T>
@@ -316,21 +693,50 @@ hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t*
 
 hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
   if (!fast) return a.bf16 ? launch_generic<bf16_t>(a, s) : launch_generic<float>(a, s);
+  const bool stream = a.x_cand_add == nullptr && a.k_cand % kStreamBK == 0 &&
+                      a.k_cand < (int64_t(1) << 22) &&
+                      ((a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN) *
+                              ((a.d_out + kStreamBM - 1) / kStreamBM) < (int64_t(1) << 31);
   if (a.k_req > 0) {
     const int tiles_d = (int)((a.d_out + 15) / 16);
     const int z_blocks = tiles_d * (int)((a.R + 15) / 16);
-    const int id_blocks = (int)((a.N + 255) / 256);
+    const int id_blocks = stream ? 0 : (int)((a.N + 255) / 256);
     hipError_t e = launch_kernel(request_gemm_bf16, dim3(z_blocks + id_blocks), dim3(256), s,
                                  static_cast<const bf16_t*>(a.x_req),
-                                 static_cast<const bf16_t*>(a.w_req), a.z, a.cand_offsets,
-                                 a.ids, (int)a.R, a.N, (int)a.k_req, (int)a.d_out, tiles_d,
-                                 z_blocks);
+                                 static_cast<const bf16_t*>(a.w_req), a.bias, a.z,
+                                 a.cand_offsets, a.ids, (int)a.R, a.N, (int)a.k_req,
+                                 (int)a.d_out, tiles_d, z_blocks);
     if (e != hipSuccess) return e;
   }
-  // Large tiles when they still give every CU at least four tiles.
+  if (stream) {
+    const int tiles_m = (int)((a.d_out + kStreamBM - 1) / kStreamBM);
+    const int64_t slots = (a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN;
+    const int64_t n_tiles = slots * tiles_m;
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    const int grid = (int)(n_tiles < cus ? n_tiles : cus);
+    const StreamStep step{grid / tiles_m, grid % tiles_m};
+    const float* zb = a.k_req > 0 ? a.z : a.bias;
+    const int32_t* off = a.k_req > 0 ? a.cand_offsets : nullptr;
+    const bf16_t* x = static_cast<const bf16_t*>(a.x_cand);
+    const bf16_t* w = static_cast<const bf16_t*>(a.w_cand);
+    bf16_t* o = static_cast<bf16_t*>(a.out);
+    auto go = [&](auto kernel) {
+      return launch_kernel(kernel, dim3((uint32_t)grid), dim3(256), s, x, w, zb, off, o,
+                           (int)a.R, a.N, (int)a.k_cand, (int)a.d_out, tiles_m, (int)slots, step);
+    };
+    if (zb != nullptr) return a.relu ? go(ikbo_gemm_stream<true, true>) : go(ikbo_gemm_stream<true, false>);
+    return a.relu ? go(ikbo_gemm_stream<false, true>) : go(ikbo_gemm_stream<false, false>);
+  }
+  // Large tiles when they still give every CU at least four tiles. The bias
+  // is already inside Z when there is a request term.
+  LinearArgs b = a;
+  if (a.k_req > 0) b.bias = nullptr;
   const int64_t big_tiles = ((a.d_out + 255) / 256) * ((a.N + 127) / 128);
-  if (big_tiles >= 1024) return launch_fast_gemm<256, 128, 32, 2, 2>(a, s);
-  return launch_fast_gemm<128, 128, 32, 2, 2>(a, s);
+  if (big_tiles >= 1024) return launch_fast_gemm<256, 128, 32, 2, 2>(b, s);
+  return launch_fast_gemm<128, 128, 32, 2, 2>(b, s);
 }
 
 }  // namespace rocs
