@@ -149,7 +149,7 @@ def timed_step_fns(p):
 
 
 _OP_KERNEL = (("dca_attention", "dca_attn_bf16"), ("glm_interaction", "glm_fm_bf16"),
-              ("", "ikbo_gemm_bf16"))
+              ("", "ikbo_gemm_stream"))
 
 
 def profiled_traffic(workload, op):

@@ -4,9 +4,11 @@
     python -m paper_2607_27744_amd.prof_summary trace  <kernel_trace.csv>
     python -m paper_2607_27744_amd.prof_summary traffic <fetch_dir> <write_dir> \
         <copy_fetch_dir> <copy_write_dir> <kernel-substring> <name>
+    python -m paper_2607_27744_amd.prof_summary copy     (run under rocprofv3 --pmc)
 
 `stats` prints the per-kernel duration table (ms) of a --kernel-trace --stats
-run. `traffic` averages FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the
+run. `copy` performs three plain 1 GiB device-to-device copies (the calibration
+workload for the counters). `traffic` averages FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the
 kernels whose name contains the substring, scales each by what the same
 counter reads for a plain device copy of known size (the calibration runs),
 and prints a JSON record with the source hash of the kernel's files, which
@@ -26,6 +28,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = {
     "dca_attn_bf16": ["csrc/attention.hip", "csrc/common.h"],
     "ikbo_gemm_bf16": ["csrc/linear.hip", "csrc/common.h"],
+    "ikbo_gemm_stream": ["csrc/linear.hip", "csrc/common.h"],
     "glm_fm_bf16": ["csrc/interaction.hip", "csrc/common.h"],
 }
 
@@ -98,8 +101,22 @@ def traffic(fetch_dir, write_dir, copy_fetch, copy_write, substring, name):
     print(json.dumps(rec, indent=1))
 
 
+def copy():
+    """Three 1 GiB bf16 device copies (hipMemcpyAsync's copy kernel)."""
+    import torch
+    n = 1 << 29
+    a = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print("copied 3 x 1 GiB", flush=True)
+
+
 if __name__ == "__main__":
-    if sys.argv[1] == "stats":
+    if sys.argv[1] == "copy":
+        copy()
+    elif sys.argv[1] == "stats":
         stats(sys.argv[2])
     elif sys.argv[1] == "trace":
         trace(sys.argv[2])
