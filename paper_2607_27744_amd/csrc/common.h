@@ -179,4 +179,12 @@ __device__ __forceinline__ void ring_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// Buffer resource over `bytes` bytes from `base` (raw, untyped: the third
+// word selects 32-bit data). A buffer load whose offset (VGPR offset plus
+// immediate) reaches past `bytes` returns zero, and such a store is dropped,
+// so a tile's edge needs no per-access branch.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 }  // namespace rocs

@@ -457,17 +457,21 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     }
   };
 
-  // Request row Zb[m0 + wm0 + 32 fm + 8 q + h4 .. +3] of the tile, loaded at
-  // the start of the tile's last slab and added in the epilogue.
+  // Request row Zb[m0 + wm0 + 32 fm + 8 q + h4 .. +3] of the tile, loaded
+  // after the tile's last MFMAs (the fragment registers are free then) and
+  // added in the epilogue. The buffer's extent is the request's row, so
+  // features past D read as zero.
   f32x4 zv[4][4];
   auto load_zb = [&](const StreamTile& c) __attribute__((always_inline)) {
     if constexpr (HAS_ZB) {
-      const float* zr = zb + (int64_t)c.r * D;
+      const auto rz = buffer_rsrc(zb + (int64_t)c.r * D, (uint32_t)D * 4u);
+      const uint32_t vo = 4u * (uint32_t)(c.m0 + wm0 + h4);
 #pragma unroll
       for (int fm = 0; fm < 4; ++fm)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          zv[fm][q] = *reinterpret_cast<const f32x4*>(zr + min(c.m0 + wm0 + 32 * fm + 8 * q + h4, D - 4));
+          zv[fm][q] = __builtin_bit_cast(
+              f32x4, __builtin_amdgcn_raw_buffer_load_b128(rz, vo + 4u * (32 * fm + 8 * q), 0, 0));
     }
   };
 
@@ -502,17 +506,22 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     const uint32_t w0 = s0[0], w2 = s0[1], w1 = s1[0], w3 = s1[1];
     return u32x4{w0, w1, w2, w3};
   };
+  // A tile inside the row range of the output stores through a buffer
+  // whose extent ends after the tile's last candidate row, so stores of rows
+  // past it are dropped. A tile that reaches past feature D (D not a
+  // multiple of the tile) tests each store.
   auto store_tile = [&](const StreamTile& c) __attribute__((always_inline)) {
-    const bool full = c.rows == BN && c.m0 + BM <= D;
-    if (full) {
+    if (c.m0 + BM <= D) {
+      const auto ro = buffer_rsrc(out + c.n0 * D, (uint32_t)c.rows * (uint32_t)D * 2u);
+      const uint32_t vo = 2u * ((uint32_t)(wn0 + l32) * (uint32_t)D + (uint32_t)(c.m0 + wm0 + 8 * hh));
 #pragma unroll
       for (int fn = 0; fn < 4; ++fn) {
-        bf16_t* orow = out + (c.n0 + wn0 + 32 * fn + l32) * D + c.m0 + wm0 + 8 * hh;
+        const uint32_t vr = vo + 64u * (uint32_t)fn * (uint32_t)D;
 #pragma unroll
         for (int fm = 0; fm < 4; ++fm)
 #pragma unroll
           for (int j = 0; j < 2; ++j)
-            *reinterpret_cast<u32x4*>(orow + 32 * fm + 16 * j) = swapped(fm, fn, j);
+            __builtin_amdgcn_raw_buffer_store_b128(swapped(fm, fn, j), ro, vr + 2u * (32 * fm + 16 * j), 0, 0);
       }
       return;
     }
@@ -559,11 +568,10 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   // One slab. Vector-memory operations retire in issue order. In an inner
   // slab the candidate loads (slab g + 2) follow the weight loads (g + 1),
   // so waiting until only those are in flight makes slab g + 1 resident. In
-  // the last slab of a tile the Zb loads go first, the candidates of slab
-  // g + 2 wait until after the epilogue, and the slab ends fully drained.
+  // the last slab of a tile the candidates of slab g + 2 wait until after
+  // the epilogue, and the Zb loads are issued and drained with the slab.
   auto step = [&](auto first_slab, auto last_slab) __attribute__((always_inline)) {
     constexpr bool kLast = decltype(last_slab)::value;
-    if constexpr (kLast) load_zb(cc);
     const bool a_next = a_queued;
     if (a_next) plan_a();
     const bool b_next = ic_live;
@@ -573,6 +581,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     cbuf_a ^= 1;
     cbuf_b = cbuf_b == NSB - 1 ? 0 : cbuf_b + 1;
     if constexpr (kLast) {
+      load_zb(cc);
       wait_vmcnt<0>();
       store_tile(cc);
       if (b_next) {
