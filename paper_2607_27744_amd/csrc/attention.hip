@@ -8,8 +8,8 @@
 // instead of once per candidate, and no candidate-batched copy exists.
 //
 // Stacking candidates: with few query tokens per candidate (one, in the
-// retrieval and ranking workloads) a tile of 256 query rows is 256/T_q
-// candidates of the same request, which fills the matrix cores the way one
+// retrieval and ranking workloads) a tile of 128 or 256 query rows holds that
+// many / T_q candidates of the same request, which fills the matrix cores the way one
 // long query sequence would (the paper co-processes 2-4 candidates per CTA for
 // the same reason, Section 4.3.2).
 //
@@ -26,7 +26,6 @@
 namespace rocs {
 namespace {
 
-constexpr int kTileRows = 256;   // query rows per workgroup (8 waves x 32)
 constexpr int kTileKeys = 64;    // history rows per K/V stage
 // Online softmax bound: a stage's weights are kept only while their per-lane
 // sum is at most 2^64 (each weight then is too); otherwise the running max
@@ -39,9 +38,14 @@ constexpr float kWeightBound = 0x1p64f;
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel (32x32x16 shape), head_dim D in {64, 128}.
 //
-// Workgroup: 8 waves x 32 query rows = one 256-row tile. With 32 rows a wave
+// Workgroup: W waves x 32 query rows = one 32 W-row tile. With 32 rows a wave
 // needs under 256 VGPRs, so two waves share each SIMD and one wave's softmax
-// (VALU) overlaps the other's matrix-core work.
+// (VALU) overlaps the other's matrix-core work. head_dim 128 takes W = 8 (a
+// 256-row tile, one workgroup per CU: 128 KiB of K/V ring). head_dim 64 takes
+// W = 4: its 64 KiB ring lets two 128-row workgroups share a CU, so one
+// workgroup's prologue (query and first K/V loads), epilogue and request
+// lookup run while the other is in its main loop, and histories of a few
+// hundred rows (a ranking request) do not leave the CU waiting on memory.
 //
 // Scores are computed transposed, S^T = K Q^T (A = K rows from LDS, B = the
 // wave's query rows held in registers for the whole history), so each lane's
@@ -70,7 +74,6 @@ constexpr float kWeightBound = 0x1p64f;
 // and the keys past the history's end are masked (weight 0) in the last,
 // ragged stage only.
 // ---------------------------------------------------------------------------
-constexpr int kAttnWaves = 8;
 constexpr int kStages = 4;       // K/V ring depth in LDS (loads run two stages ahead)
 
 // 16-byte chunk c of history row `key` (D bf16 = 2D bytes) sits at chunk
@@ -83,13 +86,16 @@ __device__ __forceinline__ int kv_swizzle(int key) {
   else return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
 }
 
-template <int D>
-__global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
+template <int D> constexpr int attn_waves() { return D == 64 ? 4 : 8; }
+
+template <int D, int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void dca_attn_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
     int64_t slots_per_head) {
-  constexpr int NT = 64 * kAttnWaves;
+  constexpr int NT = 64 * W;
+  constexpr int TR = 32 * W;           // query rows per tile
   constexpr int KB = kTileKeys / 32;   // 32-key blocks per stage
   constexpr int KS = D / 16;           // MFMA steps over head_dim
   constexpr int DB = D / 32;           // 32-wide output column blocks
@@ -98,10 +104,10 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
   constexpr int CR = D / 8;            // 16-byte chunks per row
   constexpr int STAGE = kTileKeys * ROWB;             // bytes of one K (or V) stage
   constexpr int KPI = 1024 / ROWB;                    // rows per wave-wide DMA load
-  constexpr int NI = kTileKeys / (KPI * kAttnWaves);  // DMA loads per wave, operand, stage
+  constexpr int NI = kTileKeys / (KPI * W);           // DMA loads per wave, operand, stage
   constexpr int NL = 2 * NI;                          // DMA loads per thread per stage
-  static_assert(NI >= 1 && kTileKeys % (KPI * kAttnWaves) == 0, "staging does not tile");
-  static_assert(NT == 512 && CR * 16 == ROWB, "layout");
+  static_assert(NI >= 1 && kTileKeys % (KPI * W) == 0, "staging does not tile");
+  static_assert(CR * 16 == ROWB, "layout");
   static_assert(kStages * STAGE <= 65536, "LDS offsets must fit the 16-bit immediate");
   __shared__ __attribute__((aligned(1024))) char lds[2 * kStages * STAGE];  // K ring, V ring
   ROCS_LDS char* const lds3 = (ROCS_LDS char*)lds;
@@ -112,12 +118,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void dca_attn_bf16(
   const uint32_t work = xcd_remap(blockIdx.x, gridDim.x);
   const int h = (int)(work / (uint64_t)slots_per_head);
   const int64_t slot = (int64_t)(work % (uint64_t)slots_per_head);
-  const int r = request_of_slot(cand_off, R, slot, Tq, kTileRows);
-  const int64_t j = slot - tile_base(cand_off, r, Tq, kTileRows);
+  const int r = request_of_slot(cand_off, R, slot, Tq, TR);
+  const int64_t j = slot - tile_base(cand_off, r, Tq, TR);
   const int64_t rend = (int64_t)cand_off[r + 1] * Tq;
-  const int64_t row0 = (int64_t)cand_off[r] * Tq + j * kTileRows;
+  const int64_t row0 = (int64_t)cand_off[r] * Tq + j * TR;
   if (row0 >= rend) return;                               // idle slot
-  const int rows = (int)(rend - row0 < kTileRows ? rend - row0 : kTileRows);
+  const int rows = (int)(rend - row0 < TR ? rend - row0 : TR);
   const int64_t kv0 = kv_off[r];
   const int L = kv_off[r + 1] - (int)kv0;
   const int64_t qs = (int64_t)H * D;                      // q / out row stride
@@ -444,10 +450,11 @@ __global__ __launch_bounds__(64) void dca_attn_generic(
 
 template <int D>
 hipError_t launch_fast(const AttentionArgs& a, hipStream_t s) {
-  const int64_t slots = a.R + (a.N * a.q_len + kTileRows - 1) / kTileRows;
+  constexpr int W = attn_waves<D>(), TR = 32 * W;
+  const int64_t slots = a.R + (a.N * a.q_len + TR - 1) / TR;
   const int64_t grid = slots * a.heads;
   const float scale_log2 = a.scale * 1.4426950408889634f;
-  return launch_kernel(dca_attn_bf16<D>, dim3((uint32_t)grid), dim3(64 * kAttnWaves), s,
+  return launch_kernel(dca_attn_bf16<D, W>, dim3((uint32_t)grid), dim3(64 * W), s,
                        static_cast<const bf16_t*>(a.q), static_cast<const bf16_t*>(a.k),
                        static_cast<const bf16_t*>(a.v), a.cand_offsets, a.kv_offsets,
                        static_cast<bf16_t*>(a.out), (int)a.R, a.q_len, a.heads, a.kv_stride,

@@ -83,14 +83,25 @@ __device__ __forceinline__ int64_t tile_base(const int32_t* __restrict__ off, in
   return (int64_t)r + ((int64_t)off[r] * rows_per_cand) / tile;
 }
 
+// The search is wave-parallel: each round the 64 lanes test 64 evenly spaced
+// requests of the remaining range at once, and the ballot of the monotone
+// test g(r) <= slot narrows the range 64-fold (two rounds of loads for up to
+// 4096 requests instead of twelve dependent ones). Call it with every lane of
+// the wave active; the result is wave-uniform.
 __device__ __forceinline__ int request_of_slot(const int32_t* __restrict__ off, int R,
                                                int64_t slot, int rows_per_cand, int tile) {
-  int lo = 0, hi = R - 1;
-  while (lo < hi) {
-    int mid = (lo + hi + 1) >> 1;
-    if (tile_base(off, mid, rows_per_cand, tile) <= slot) lo = mid; else hi = mid - 1;
+  const int lane = (int)(threadIdx.x & 63);
+  int lo = 0, n = R;                      // answer in [lo, lo + n); g(lo) <= slot holds
+  while (n > 1) {
+    const int step = (n + 63) / 64;
+    const int r = lo + lane * step;
+    const bool ok = r < lo + n && tile_base(off, r, rows_per_cand, tile) <= slot;
+    const uint64_t m = __ballot(ok);      // lanes 0 .. k set, k the last request that fits
+    const int k = 63 - __builtin_clzll(m);
+    lo += k * step;
+    n = min(step, n - k * step);
   }
-  return lo;
+  return __builtin_amdgcn_readfirstlane(lo);
 }
 
 // Workgroups are dispatched round-robin over the XCDs (workgroup b runs on
