@@ -116,6 +116,36 @@ int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req,
 
 /*
  * ---------------------------------------------------------------------------
+ * rocs_ikbo_linear_mapped: rocs_ikbo_linear with the index map m given as a
+ * per-candidate request id instead of CSR offsets (Section 4.1 defines m as
+ * any map {0..B_c-1} -> {0..B_r-1}; candidates of one request need not be
+ * contiguous or ordered).
+ *
+ *   cand_request_ids [N] int32, device memory: m_n for every candidate n,
+ *                    each in [0, R). Trusted device data like the offsets: an
+ *                    id outside [0, R) gives wrong rows for that candidate
+ *                    (the kernels clamp it into range), never an access
+ *                    outside the request-side product. May be NULL iff
+ *                    k_req == 0.
+ * Every other argument, the result, the workspace (at least
+ * rocs_ikbo_linear_workspace_size() bytes) and the errors are those of
+ * rocs_ikbo_linear. The request-side product is still formed once per
+ * request. The candidate GEMM resolves m per row in its epilogue (a tile
+ * whose rows share one request loads Z once), so it runs the kernel with a
+ * per-row request lookup rather than the request-aligned streaming kernel.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_ikbo_linear_mapped(const void* x_req, int64_t k_req,
+                                const void* x_cand, const void* x_cand_add, int64_t k_cand,
+                                const void* w_req, const void* w_cand, const float* bias,
+                                const int32_t* cand_request_ids,
+                                int64_t num_requests, int64_t num_cand, int64_t d_out,
+                                int32_t dtype, int32_t activation,
+                                void* out, void* workspace, size_t workspace_bytes,
+                                void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * rocs_dca_attention: candidate-side Deep Cross Attention
  * A^C = Attn(Q^C, S W_K, S W_V) (Section 3.2, Eq. dca-attention) with the
  * request-batched K/V consumed directly (Section 4.3.1): every candidate of
@@ -149,6 +179,30 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
                            int32_t q_len, int32_t num_heads, int32_t head_dim,
                            int64_t kv_row_stride, float softmax_scale, int32_t dtype,
                            void* out, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_dca_attention_mapped: rocs_dca_attention with the index map m given as
+ * a per-candidate request id (Section 4.3.1: the kernel resolves m_i before
+ * loading candidate i's K/V; here m need not keep a request's candidates
+ * contiguous).
+ *
+ *   cand_request_ids [N] int32, device memory, each in [0, R) (trusted; an
+ *                    id outside the range is clamped into it, so it gives
+ *                    wrong rows, never an access outside kv_offsets).
+ * Every other argument, the result and the errors are those of
+ * rocs_dca_attention. Request tiles need contiguous candidates, so this
+ * entry point runs the general kernel (one wave per query row and head,
+ * history read through L2); reorder candidates by request and use
+ * rocs_dca_attention for throughput.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_dca_attention_mapped(const void* q, const void* k, const void* v,
+                                  const int32_t* cand_request_ids, const int32_t* kv_offsets,
+                                  int64_t num_requests, int64_t num_cand,
+                                  int32_t q_len, int32_t num_heads, int32_t head_dim,
+                                  int64_t kv_row_stride, float softmax_scale, int32_t dtype,
+                                  void* out, void* stream);
 
 /*
  * ---------------------------------------------------------------------------

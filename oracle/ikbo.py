@@ -2,8 +2,10 @@
 
 Notation follows the paper. A batch holds R requests (batch size B_r) and N
 candidates (B_c). The index map m of Section 4.1 sends candidate i to its
-request m_i; here it arrives as CSR offsets: candidate n belongs to request r
-iff cand_offsets[r] <= n < cand_offsets[r + 1].
+request m_i. It arrives as CSR offsets (candidate n belongs to request r iff
+cand_offsets[r] <= n < cand_offsets[r + 1], so a request's candidates are
+contiguous), or, where an operator takes `request_map`, as m itself: one
+request index per candidate, in any order.
 
 Weights follow Eq. glm-linear: a block W_ij maps input group j to output group
 i and has shape [out, in], so a batch of row vectors is multiplied by W^T.
@@ -22,7 +24,7 @@ import math
 import numpy as np
 
 __all__ = [
-    "request_ids", "check_offsets", "activation",
+    "request_ids", "check_offsets", "resolve_map", "activation",
     "ikbo_linear", "ikbo_linear_decomposed", "linear",
     "sequence_projection", "dca_attention",
     "glm_fm", "glm_fm_masked_blocks", "amortized_flops",
@@ -56,6 +58,19 @@ def request_ids(cand_offsets):
     return np.repeat(np.arange(counts.size, dtype=np.int64), counts)
 
 
+def resolve_map(cand_offsets, request_map, n_cand, n_req):
+    """m_i for every candidate: given directly (request_map, any order), else
+    expanded from the CSR offsets. Every m_i must name one of the n_req requests."""
+    if request_map is None:
+        return request_ids(check_offsets(cand_offsets, n_cand))
+    m = np.asarray(request_map, dtype=np.int64)
+    if m.shape != (n_cand,):
+        raise ValueError(f"request_map must hold one entry per candidate ({n_cand})")
+    if m.size and (m.min() < 0 or m.max() >= n_req):
+        raise ValueError("request_map entries must lie in [0, R)")
+    return m
+
+
 def activation(x, act):
     """Unary pointwise activation (GLM-compliant, Eq. glm-elementwise)."""
     if act in (None, "none"):
@@ -74,7 +89,7 @@ def _f64(a):
 # ---------------------------------------------------------------------------
 
 def ikbo_linear(x_req, x_cand, w_req, w_cand, bias, cand_offsets, act="none",
-                rows=None, chunk=_CHUNK):
+                rows=None, chunk=_CHUNK, request_map=None):
     """Candidate-side output of a two-group GLM linear, by explicit broadcast.
 
     y^C = act(W_CR x^R + W_CC x^C + b^C) (Eq. glm-linear, output group 1; the
@@ -85,6 +100,7 @@ def ikbo_linear(x_req, x_cand, w_req, w_cand, bias, cand_offsets, act="none",
     x_req [R, K_r], x_cand [N, K_c], w_req [D, K_r], w_cand [D, K_c],
     bias [D] or None. K_r may be 0 (then this is a plain linear layer).
     rows: optional candidate indices; only those outputs are computed.
+    request_map: m given per candidate instead of cand_offsets.
     Returns float64 [N, D] (or [len(rows), D]).
     """
     x_cand = np.asarray(x_cand)          # converted chunk by chunk below
@@ -95,7 +111,7 @@ def ikbo_linear(x_req, x_cand, w_req, w_cand, bias, cand_offsets, act="none",
     if k_req:
         x_req = _f64(x_req)
         w_req = _f64(w_req)
-        m = request_ids(check_offsets(cand_offsets, n_cand))
+        m = resolve_map(cand_offsets, request_map, n_cand, x_req.shape[0])
         w_full = np.concatenate([w_req, w_cand], axis=1)    # [D, K_r + K_c]
     else:
         m = None
@@ -154,7 +170,8 @@ def _softmax_rows(scores):
 
 
 def dca_attention(q, k, v, cand_offsets, kv_offsets, scale=None,
-                  mode="explicit", rows=None, q_subset=False, chunk=4096):
+                  mode="explicit", rows=None, q_subset=False, chunk=4096,
+                  request_map=None):
     """Candidate-side cross attention A^C = Attn(Q^C, K_{m_i}, V_{m_i}).
 
     q [N, T, H, d] (T query tokens per candidate), k and v [L_total, H, d]
@@ -174,13 +191,19 @@ def dca_attention(q, k, v, cand_offsets, kv_offsets, scale=None,
     rows: optional candidate indices; only those outputs are computed. With
     q_subset=True, q holds only those candidates' queries (q[i] is candidate
     rows[i]); otherwise q covers all N candidates.
+    request_map: m given per candidate (any order) instead of cand_offsets.
     """
     q = np.asarray(q)
-    cand_off = check_offsets(cand_offsets)
-    n_cand = int(cand_off[-1])
     _, t_q, n_heads, d = q.shape
     kv_off = check_offsets(kv_offsets, np.asarray(k).shape[0])
-    m = request_ids(cand_off)
+    if request_map is not None:
+        n_cand = len(request_map)
+        m = resolve_map(None, request_map, n_cand, kv_off.size - 1)
+        cand_offsets = np.zeros(kv_off.size, dtype=np.int64)   # only its length is used
+    else:
+        cand_off = check_offsets(cand_offsets)
+        n_cand = int(cand_off[-1])
+        m = request_ids(cand_off)
     if q_subset:
         if rows is None or len(rows) != q.shape[0]:
             raise ValueError("q_subset needs rows with one entry per query")

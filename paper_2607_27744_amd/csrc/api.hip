@@ -72,11 +72,19 @@ size_t rocs_ikbo_linear_workspace_size(int64_t num_requests, int64_t num_cand, i
          align256((size_t)num_cand * sizeof(int32_t));
 }
 
-int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
-                         const void* x_cand_add, int64_t k_cand, const void* w_req,
-                         const void* w_cand, const float* bias, const int32_t* cand_offsets,
-                         int64_t R, int64_t N, int64_t d_out, int32_t dtype, int32_t activation,
-                         void* out, void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared by rocs_ikbo_linear (CSR offsets) and rocs_ikbo_linear_mapped (a
+// per-candidate request map, `mapped`): only one of cand_offsets / cand_ids
+// is read.
+int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_req,
+                    const void* x_cand, const void* x_cand_add, int64_t k_cand,
+                    const void* w_req, const void* w_cand, const float* bias,
+                    const int32_t* cand_offsets, const int32_t* cand_ids, int64_t R, int64_t N,
+                    int64_t d_out, int32_t dtype, int32_t activation, void* out,
+                    void* workspace, size_t workspace_bytes, void* stream) {
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (activation != ROCS_ACT_NONE && activation != ROCS_ACT_RELU)
     return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown activation %d", activation);
@@ -93,9 +101,10 @@ int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
     return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests to own them");
   if (x_cand == nullptr || w_cand == nullptr || out == nullptr)
     return fail(ROCS_ERR_INVALID_ARGUMENT, "x_cand, w_cand and out must not be NULL");
-  if (k_req > 0 && (x_req == nullptr || w_req == nullptr || cand_offsets == nullptr))
-    return fail(ROCS_ERR_INVALID_ARGUMENT,
-                "k_req > 0 needs x_req, w_req and cand_offsets");
+  if (k_req > 0 && (x_req == nullptr || w_req == nullptr ||
+                    (mapped ? cand_ids == nullptr : cand_offsets == nullptr)))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "k_req > 0 needs x_req, w_req and %s",
+                mapped ? "cand_request_ids" : "cand_offsets");
   const size_t need = rocs_ikbo_linear_workspace_size(R, N, d_out, k_req);
   if (need > 0) {
     if (workspace == nullptr || workspace_bytes < need)
@@ -114,6 +123,7 @@ int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
       {w_cand, (size_t)d_out * k_cand * es, "w_cand"},
       {bias, (size_t)d_out * sizeof(float), "bias"},
       {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"},
+      {cand_ids, (size_t)N * sizeof(int32_t), "cand_request_ids"},
       {need > 0 ? workspace : nullptr, need, "workspace"},
   };
   for (const auto& in : ins)
@@ -124,7 +134,8 @@ int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
     const struct { const void* p; size_t n; const char* name; } inw[] = {
         {x_req, (size_t)R * k_req * es, "x_req"}, {x_cand, (size_t)N * k_cand * es, "x_cand"},
         {w_req, (size_t)d_out * k_req * es, "w_req"}, {w_cand, (size_t)d_out * k_cand * es, "w_cand"},
-        {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"}};
+        {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"},
+        {cand_ids, (size_t)N * sizeof(int32_t), "cand_request_ids"}};
     for (const auto& in : inw)
       if (overlap(workspace, need, in.p, in.n))
         return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace overlaps %s", in.name);
@@ -140,23 +151,56 @@ int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
   a.out = out;
   if (need > 0) {
     a.z = static_cast<float*>(workspace);
-    a.ids = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) +
-                                       align256((size_t)R * d_out * sizeof(float)));
+    a.ids = mapped ? const_cast<int32_t*>(cand_ids)
+                   : reinterpret_cast<int32_t*>(static_cast<char*>(workspace) +
+                                                align256((size_t)R * d_out * sizeof(float)));
+    a.ids_given = mapped;
   }
   const bool fast = a.bf16 && k_cand % 8 == 0 && k_req % 8 == 0 && d_out % 4 == 0 &&
                     aligned(x_cand, 16) && aligned(x_cand_add, 16) && aligned(w_cand, 16) &&
                     aligned(x_req, 16) && aligned(w_req, 16) && aligned(bias, 16) &&
                     aligned(out, 16);
   const hipError_t e = rocs::launch_linear(a, fast, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_ikbo_linear: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
   return ok();
 }
 
-int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
-                           const int32_t* cand_offsets, const int32_t* kv_offsets, int64_t R,
-                           int64_t N, int32_t q_len, int32_t num_heads, int32_t head_dim,
-                           int64_t kv_row_stride, float softmax_scale, int32_t dtype, void* out,
-                           void* stream) {
+}  // namespace
+
+extern "C" {
+
+int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
+                         const void* x_cand_add, int64_t k_cand, const void* w_req,
+                         const void* w_cand, const float* bias, const int32_t* cand_offsets,
+                         int64_t R, int64_t N, int64_t d_out, int32_t dtype, int32_t activation,
+                         void* out, void* workspace, size_t workspace_bytes, void* stream) {
+  return linear_impl("rocs_ikbo_linear", false, x_req, k_req, x_cand, x_cand_add, k_cand,
+                     w_req, w_cand, bias, cand_offsets, nullptr, R, N, d_out, dtype, activation,
+                     out, workspace, workspace_bytes, stream);
+}
+
+int32_t rocs_ikbo_linear_mapped(const void* x_req, int64_t k_req, const void* x_cand,
+                                const void* x_cand_add, int64_t k_cand, const void* w_req,
+                                const void* w_cand, const float* bias,
+                                const int32_t* cand_request_ids, int64_t R, int64_t N,
+                                int64_t d_out, int32_t dtype, int32_t activation, void* out,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  return linear_impl("rocs_ikbo_linear_mapped", true, x_req, k_req, x_cand, x_cand_add,
+                     k_cand, w_req, w_cand, bias, nullptr, cand_request_ids, R, N, d_out, dtype,
+                     activation, out, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Shared by rocs_dca_attention (CSR cand_offsets) and rocs_dca_attention_mapped
+// (a per-candidate request map, `mapped`): only one of the two is read.
+int32_t attention_impl(const char* name, bool mapped, const void* q, const void* k,
+                       const void* v, const int32_t* cand_offsets, const int32_t* cand_ids,
+                       const int32_t* kv_offsets, int64_t R, int64_t N, int32_t q_len,
+                       int32_t num_heads, int32_t head_dim, int64_t kv_row_stride,
+                       float softmax_scale, int32_t dtype, void* out, void* stream) {
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (R < 0 || N < 0 || q_len < 1 || num_heads < 1 || head_dim < 1 || kv_row_stride < 0)
     return fail(ROCS_ERR_INVALID_ARGUMENT,
@@ -172,14 +216,15 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
     return fail(ROCS_ERR_UNSUPPORTED, "batch too large");
   if (N == 0) return ok();
   if (R == 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests");
-  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || cand_offsets == nullptr ||
-      kv_offsets == nullptr)
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || kv_offsets == nullptr ||
+      (mapped ? cand_ids == nullptr : cand_offsets == nullptr))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
   const size_t es = esize(dtype);
   const size_t out_bytes = (size_t)N * q_len * row_elems * es;
   if (overlap(out, out_bytes, q, out_bytes) || overlap(out, out_bytes, k, 1) ||
       overlap(out, out_bytes, v, 1) ||
       overlap(out, out_bytes, cand_offsets, (size_t)(R + 1) * 4) ||
+      overlap(out, out_bytes, cand_ids, (size_t)N * 4) ||
       overlap(out, out_bytes, kv_offsets, (size_t)(R + 1) * 4))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "out overlaps an input");
 
@@ -190,12 +235,37 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
   a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf((float)head_dim);
   a.bf16 = dtype == ROCS_DTYPE_BF16;
   a.out = out;
+  a.ids = mapped ? cand_ids : nullptr;
   const bool fast = a.bf16 && (head_dim == 64 || head_dim == 128) && stride % 8 == 0 &&
                     stride < (int64_t(1) << 24) &&
                     aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16);
   const hipError_t e = rocs::launch_attention(a, fast, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_dca_attention: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
+                           const int32_t* cand_offsets, const int32_t* kv_offsets, int64_t R,
+                           int64_t N, int32_t q_len, int32_t num_heads, int32_t head_dim,
+                           int64_t kv_row_stride, float softmax_scale, int32_t dtype, void* out,
+                           void* stream) {
+  return attention_impl("rocs_dca_attention", false, q, k, v, cand_offsets, nullptr,
+                        kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
+                        softmax_scale, dtype, out, stream);
+}
+
+int32_t rocs_dca_attention_mapped(const void* q, const void* k, const void* v,
+                                  const int32_t* cand_request_ids, const int32_t* kv_offsets,
+                                  int64_t R, int64_t N, int32_t q_len, int32_t num_heads,
+                                  int32_t head_dim, int64_t kv_row_stride, float softmax_scale,
+                                  int32_t dtype, void* out, void* stream) {
+  return attention_impl("rocs_dca_attention_mapped", true, q, k, v, nullptr, cand_request_ids,
+                        kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
+                        softmax_scale, dtype, out, stream);
 }
 
 int32_t rocs_glm_interaction(const void* x_req, const void* x_cand, const int32_t* cand_offsets,

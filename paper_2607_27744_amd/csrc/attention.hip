@@ -404,10 +404,15 @@ template <typename T>
 __global__ __launch_bounds__(64) void dca_attn_generic(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
-    T* __restrict__ out, int R, int Tq, int H, int D, int64_t kv_stride, float scale) {
+    T* __restrict__ out, int R, int Tq, int H, int D, int64_t kv_stride, float scale,
+    const int32_t* __restrict__ ids) {
   const int64_t row = blockIdx.x;
   const int h = blockIdx.y, lane = threadIdx.x;
-  const int r = owner_of(cand_off, R, row / Tq);
+  // The request: from the caller's per-candidate map (clamped into [0, R),
+  // so a malformed map gives wrong rows, never an access outside the
+  // offsets), else from the CSR offsets.
+  const int r = ids != nullptr ? (int)min((uint32_t)ids[row / Tq], (uint32_t)(R - 1))
+                               : owner_of(cand_off, R, row / Tq);
   const int64_t a = kv_off[r];
   const int L = kv_off[r + 1] - (int)a;
   const int64_t qo = (row * H + h) * D;
@@ -467,13 +472,16 @@ hipError_t launch_generic(const AttentionArgs& a, hipStream_t s) {
                        dim3(64), s, static_cast<const T*>(a.q), static_cast<const T*>(a.k),
                        static_cast<const T*>(a.v), a.cand_offsets, a.kv_offsets,
                        static_cast<T*>(a.out), (int)a.R, a.q_len, a.heads, a.head_dim,
-                       a.kv_stride, a.scale);
+                       a.kv_stride, a.scale, a.ids);
 }
 
 }  // namespace
 
 hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s) {
-  if (fast) return a.head_dim == 128 ? launch_fast<128>(a, s) : launch_fast<64>(a, s);
+  // The tiled kernel needs the candidates of a request contiguous (CSR); a
+  // caller's per-candidate map runs the general kernel.
+  if (fast && a.ids == nullptr)
+    return a.head_dim == 128 ? launch_fast<128>(a, s) : launch_fast<64>(a, s);
   return a.bf16 ? launch_generic<bf16_t>(a, s) : launch_generic<float>(a, s);
 }
 

@@ -18,7 +18,8 @@ struct LinearArgs {
   bool bf16, relu;
   void* out;
   float* z;          // [R, d_out] workspace (k_req > 0)
-  int32_t* ids;      // [N] workspace (k_req > 0)
+  int32_t* ids;      // [N] request of each candidate: workspace, or the caller's map
+  bool ids_given;    // ids is the caller's map (no CSR offsets, no expansion)
 };
 
 struct AttentionArgs {
@@ -33,6 +34,7 @@ struct AttentionArgs {
   float scale;
   bool bf16;
   void* out;
+  const int32_t* ids;  // caller's per-candidate request map, or NULL (CSR offsets)
 };
 
 struct InteractionArgs {

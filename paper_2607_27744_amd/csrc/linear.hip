@@ -95,7 +95,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) __attribute__((amdgpu_waves
 void ikbo_gemm_bf16(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ xadd, const bf16_t* __restrict__ w,
     const float* __restrict__ bias, const float* __restrict__ z, const int32_t* __restrict__ ids,
-    bf16_t* __restrict__ out, int64_t N, int K, int D, int tiles_m, int relu) {
+    bf16_t* __restrict__ out, int64_t N, int K, int D, int tiles_m, int relu, int R,
+    int ids_sorted) {
   constexpr int NT = 64 * WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
   constexpr int FM = WM / 32, FN = WN / 32;
@@ -158,13 +159,19 @@ void ikbo_gemm_bf16(
   // is feature m0 + wm0 + 32 fm + 8 q + h4 + i of candidate n0 + wn0 + 32 fn + l32.
   f32x16 acc[FM][FN];
   {
-    const bool one_request = z != nullptr && ids[n0] == ids[(n0 + BN < N ? n0 + BN : N) - 1];
+    // A request id outside [0, R) (a malformed caller map) is clamped into
+    // range: wrong rows, never an access outside Z.
+    auto req = [&](int64_t n) { return (int)min((uint32_t)ids[n], (uint32_t)(R - 1)); };
+    // Sorted ids (expanded from CSR offsets): equal first and last ids mean
+    // the whole tile has one request. A caller's map has no such order.
+    const bool one_request = z != nullptr && ids_sorted != 0 &&
+                             ids[n0] == ids[(n0 + BN < N ? n0 + BN : N) - 1];
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn) {
       const int64_t n = n0 + wn0 + 32 * fn + l32;
       const float* zr = nullptr;
       if (z != nullptr) {
-        const int r = one_request ? ids[n0] : (n < N ? ids[n] : 0);
+        const int r = one_request ? req(n0) : (n < N ? req(n) : 0);
         zr = z + (int64_t)r * D;
       }
 #pragma unroll
@@ -634,7 +641,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void linear_generic(
     const T* __restrict__ x, const T* __restrict__ xadd, const T* __restrict__ w,
     const float* __restrict__ bias, const float* __restrict__ z, const int32_t* __restrict__ ids,
-    T* __restrict__ out, int64_t N, int K, int D, int relu) {
+    T* __restrict__ out, int64_t N, int K, int D, int relu, int R) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= N * D) return;
   const int64_t n = idx / D;
@@ -645,7 +652,7 @@ __global__ __launch_bounds__(256) void linear_generic(
     if (xadd != nullptr) xv = (float)from_f32<T>(xv + load_f32(xadd + n * K + k));
     acc = fmaf(xv, load_f32(w + (int64_t)d * K + k), acc);
   }
-  if (z != nullptr) acc += z[(int64_t)ids[n] * D + d];
+  if (z != nullptr) acc += z[(int64_t)min((uint32_t)ids[n], (uint32_t)(R - 1)) * D + d];
   if (bias != nullptr) acc += bias[d];
   if (relu) acc = fmaxf(acc, 0.f);
   out[idx] = from_f32<T>(acc);
@@ -665,11 +672,11 @@ hipError_t launch_fast_gemm(const LinearArgs& a, hipStream_t s) {
     return launch_kernel(ikbo_gemm_bf16<BM, BN, BK, WMW, WNW, true>, dim3((uint32_t)grid),
                          dim3(64 * WMW * WNW), s,
                          x, xa, w, a.bias, z, a.ids, o, a.N, (int)a.k_cand, (int)a.d_out,
-                         tiles_m, (int)a.relu);
+                         tiles_m, (int)a.relu, (int)a.R, (int)!a.ids_given);
   return launch_kernel(ikbo_gemm_bf16<BM, BN, BK, WMW, WNW, false>, dim3((uint32_t)grid),
                        dim3(64 * WMW * WNW), s,
                        x, xa, w, a.bias, z, a.ids, o, a.N, (int)a.k_cand, (int)a.d_out,
-                       tiles_m, (int)a.relu);
+                       tiles_m, (int)a.relu, (int)a.R, (int)!a.ids_given);
 }
 
 template <typename T>
@@ -677,7 +684,7 @@ hipError_t launch_generic(const LinearArgs& a, hipStream_t s) {
   hipError_t e = hipSuccess;
   if (a.k_req > 0) {
     const int z_blocks = (int)((a.R * a.d_out + 255) / 256);
-    const int id_blocks = (int)((a.N + 255) / 256);
+    const int id_blocks = a.ids_given ? 0 : (int)((a.N + 255) / 256);
     e = launch_kernel(request_gemm_generic<T>, dim3(z_blocks + id_blocks), dim3(256), s,
                       static_cast<const T*>(a.x_req), static_cast<const T*>(a.w_req), a.z,
                       a.cand_offsets, a.ids, (int)a.R, a.N, (int)a.k_req, (int)a.d_out,
@@ -689,7 +696,7 @@ hipError_t launch_generic(const LinearArgs& a, hipStream_t s) {
                        static_cast<const T*>(a.x_cand), static_cast<const T*>(a.x_cand_add),
                        static_cast<const T*>(a.w_cand), a.bias,
                        a.k_req > 0 ? a.z : nullptr, a.ids, static_cast<T*>(a.out), a.N,
-                       (int)a.k_cand, (int)a.d_out, (int)a.relu);
+                       (int)a.k_cand, (int)a.d_out, (int)a.relu, (int)a.R);
 }
 
 }  // namespace
@@ -702,14 +709,16 @@ hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t*
 
 hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
   if (!fast) return a.bf16 ? launch_generic<bf16_t>(a, s) : launch_generic<float>(a, s);
-  const bool stream = a.x_cand_add == nullptr && a.k_cand % kStreamBK == 0 &&
+  // The streaming kernel needs request-aligned tiles, i.e. CSR offsets; a
+  // caller's per-candidate map takes the kernel with per-row request lookup.
+  const bool stream = !a.ids_given && a.x_cand_add == nullptr && a.k_cand % kStreamBK == 0 &&
                       a.k_cand < (int64_t(1) << 22) &&
                       ((a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN) *
                               ((a.d_out + kStreamBM - 1) / kStreamBM) < (int64_t(1) << 31);
   if (a.k_req > 0) {
     const int tiles_d = (int)((a.d_out + 15) / 16);
     const int z_blocks = tiles_d * (int)((a.R + 15) / 16);
-    const int id_blocks = stream ? 0 : (int)((a.N + 255) / 256);
+    const int id_blocks = stream || a.ids_given ? 0 : (int)((a.N + 255) / 256);
     hipError_t e = launch_kernel(request_gemm_bf16, dim3(z_blocks + id_blocks), dim3(256), s,
                                  static_cast<const bf16_t*>(a.x_req),
                                  static_cast<const bf16_t*>(a.w_req), a.bias, a.z,

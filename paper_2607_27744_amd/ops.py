@@ -14,8 +14,9 @@ import torch
 from . import _lib
 
 __all__ = [
-    "load_library", "ikbo_linear", "linear_workspace_size", "dca_attention",
-    "glm_interaction", "request_ids", "validate_offsets", "RocsError",
+    "load_library", "ikbo_linear", "ikbo_linear_mapped", "linear_workspace_size",
+    "dca_attention", "dca_attention_mapped", "dca_request_attention", "glm_interaction",
+    "request_ids", "validate_offsets", "RocsError",
 ]
 
 RocsError = _lib.RocsError
@@ -64,6 +65,12 @@ def _offsets(off, n_req):
     _need(off.numel() == n_req + 1, f"offsets need {n_req + 1} entries, got {off.numel()}")
 
 
+def _request_map(ids, n_cand):
+    _need(ids.dtype == torch.int32 and ids.dim() == 1 and ids.is_contiguous(),
+          "cand_request_ids must be a contiguous 1-D int32 tensor")
+    _need(ids.numel() == n_cand, f"cand_request_ids needs {n_cand} entries, got {ids.numel()}")
+
+
 def linear_workspace_size(num_requests, num_cand, d_out, k_req):
     return int(_lib.load().rocs_ikbo_linear_workspace_size(num_requests, num_cand, d_out, k_req))
 
@@ -75,6 +82,21 @@ def ikbo_linear(x_cand, w_cand, *, x_req=None, w_req=None, cand_offsets=None, bi
     x_cand [N, K_c], w_cand [D, K_c], x_req [R, K_r], w_req [D, K_r] (paper's [out, in]
     orientation), cand_offsets [R + 1] int32, bias [D] float32.
     """
+    return _linear(x_cand, w_cand, x_req, w_req, cand_offsets, None, None, bias, activation,
+                   x_cand_add, out, workspace, stream)
+
+
+def ikbo_linear_mapped(x_cand, w_cand, *, x_req=None, w_req=None, cand_request_ids=None,
+                       bias=None, activation="none", x_cand_add=None, out=None,
+                       workspace=None, stream=None):
+    """rocs_ikbo_linear_mapped: as ikbo_linear, with m given per candidate
+    (cand_request_ids int32 [N], each in [0, R) with R = x_req.shape[0])."""
+    return _linear(x_cand, w_cand, x_req, w_req, None, cand_request_ids, True, bias,
+                   activation, x_cand_add, out, workspace, stream)
+
+
+def _linear(x_cand, w_cand, x_req, w_req, cand_offsets, cand_ids, mapped, bias, activation,
+            x_cand_add, out, workspace, stream):
     lib = _lib.load()
     _need(x_cand.dim() == 2 and w_cand.dim() == 2, "x_cand and w_cand must be 2-D")
     n_cand, k_cand = x_cand.shape
@@ -83,16 +105,20 @@ def ikbo_linear(x_cand, w_cand, *, x_req=None, w_req=None, cand_offsets=None, bi
     code = _dtype_code(x_cand)
     for t in (w_cand, x_req, w_req, x_cand_add):
         _need(t is None or t.dtype == x_cand.dtype, "inputs must share one dtype")
+    index = cand_ids if mapped else cand_offsets
     if x_req is not None:
-        _need(w_req is not None and cand_offsets is not None,
-              "x_req needs w_req and cand_offsets")
+        _need(w_req is not None and index is not None,
+              "x_req needs w_req and " + ("cand_request_ids" if mapped else "cand_offsets"))
         _need(x_req.dim() == 2 and w_req.dim() == 2, "x_req and w_req must be 2-D")
         n_req, k_req = x_req.shape
         _need(w_req.shape == (d_out, k_req), "w_req must be [d_out, k_req]")
     else:
         k_req = 0
-        n_req = 0 if cand_offsets is None else cand_offsets.numel() - 1
-    if cand_offsets is not None:
+        n_req = 0 if mapped or cand_offsets is None else cand_offsets.numel() - 1
+    if mapped:
+        if cand_ids is not None:
+            _request_map(cand_ids, n_cand)
+    elif cand_offsets is not None:
         _offsets(cand_offsets, n_req)
     if x_cand_add is not None:
         _need(x_cand_add.shape == x_cand.shape, "x_cand_add must match x_cand")
@@ -107,20 +133,45 @@ def ikbo_linear(x_cand, w_cand, *, x_req=None, w_req=None, cand_offsets=None, bi
     need = int(lib.rocs_ikbo_linear_workspace_size(n_req, n_cand, d_out, k_req))
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=x_cand.device)
-    _on_gpu(x_cand, w_cand, x_req, w_req, cand_offsets, bias, x_cand_add, out, workspace)
+    _on_gpu(x_cand, w_cand, x_req, w_req, index, bias, x_cand_add, out, workspace)
     _need(activation in _ACT, f"activation must be one of {sorted(k for k in _ACT if k)}")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _lib.check(lib.rocs_ikbo_linear(
+    fn, name = ((lib.rocs_ikbo_linear_mapped, "rocs_ikbo_linear_mapped") if mapped
+                else (lib.rocs_ikbo_linear, "rocs_ikbo_linear"))
+    _lib.check(fn(
         _ptr(x_req), k_req, _ptr(x_cand), _ptr(x_cand_add), k_cand, _ptr(w_req), _ptr(w_cand),
-        _ptr(bias), _ptr(cand_offsets), n_req, n_cand, d_out, code, _ACT[activation],
-        _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)), "rocs_ikbo_linear")
+        _ptr(bias), _ptr(index), n_req, n_cand, d_out, code, _ACT[activation],
+        _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)), name)
     return out
 
 
 def dca_attention(q, k, v, cand_offsets, kv_offsets, *, scale=None, out=None, stream=None):
     """Candidate-side DCA: q [N, T, H, d]; k, v [L_total, H, d] (rows may be strided,
     e.g. column slices of one [L, 2 H d] projection); offsets int32 [R + 1]."""
+    return _attention(q, k, v, cand_offsets, None, kv_offsets, scale, out, stream)
+
+
+def dca_attention_mapped(q, k, v, cand_request_ids, kv_offsets, *, scale=None, out=None,
+                         stream=None):
+    """rocs_dca_attention_mapped: as dca_attention, with m given per candidate
+    (cand_request_ids int32 [N], each in [0, R) with R = kv_offsets.numel() - 1)."""
+    return _attention(q, k, v, None, cand_request_ids, kv_offsets, scale, out, stream)
+
+
+def dca_request_attention(q_req, k, v, kv_offsets, *, scale=None, out=None, stream=None):
+    """Request-side cross attention A^R = Attn(Q^R, K, V) (Eq. dca-attention): request r's
+    queries q_req[r] [T, H, d] attend over r's own history. The identity map (request r is
+    its own single "candidate") on rocs_dca_attention; the offsets are built on the device."""
+    _need(q_req.dim() == 4, "q_req must be [R, T, H, d]")
+    n_req = q_req.shape[0]
+    _need(kv_offsets.numel() == n_req + 1, "kv_offsets needs R + 1 entries")
+    ident = torch.arange(n_req + 1, dtype=torch.int32, device=q_req.device)
+    return _attention(q_req, k, v, ident, None, kv_offsets, scale, out, stream)
+
+
+def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream):
     lib = _lib.load()
+    mapped = cand_ids is not None
     _need(q.dim() == 4 and q.is_contiguous(), "q must be a contiguous [N, T, H, d] tensor")
     n_cand, q_len, heads, dim = q.shape
     _need(k.dim() == 3 and v.dim() == 3 and k.shape == v.shape, "k and v must be [L, H, d]")
@@ -130,19 +181,24 @@ def dca_attention(q, k, v, cand_offsets, kv_offsets, *, scale=None, out=None, st
     _need(k.stride(0) == v.stride(0), "k and v must share a row stride")
     for t in (k, v):
         _need(t.dtype == q.dtype, "q, k, v must share one dtype")
-    n_req = cand_offsets.numel() - 1
-    _offsets(cand_offsets, n_req)
+    n_req = kv_offsets.numel() - 1
     _offsets(kv_offsets, n_req)
+    if mapped:
+        _request_map(cand_ids, n_cand)
+    else:
+        _offsets(cand_offsets, n_req)
     if out is None:
         out = torch.empty_like(q)
     _need(out.shape == q.shape and out.dtype == q.dtype and out.is_contiguous(),
           "out must match q")
-    _on_gpu(q, k, v, cand_offsets, kv_offsets, out)
+    _on_gpu(q, k, v, cand_offsets, cand_ids, kv_offsets, out)
     stride = k.stride(0) if k.shape[0] > 1 else heads * dim
-    _lib.check(lib.rocs_dca_attention(
-        _ptr(q), _ptr(k), _ptr(v), _ptr(cand_offsets), _ptr(kv_offsets), n_req, n_cand,
-        q_len, heads, dim, stride, float(scale or 0.0), _dtype_code(q), _ptr(out),
-        _stream(stream)), "rocs_dca_attention")
+    fn, name = ((lib.rocs_dca_attention_mapped, "rocs_dca_attention_mapped") if mapped
+                else (lib.rocs_dca_attention, "rocs_dca_attention"))
+    _lib.check(fn(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(cand_ids if mapped else cand_offsets), _ptr(kv_offsets),
+        n_req, n_cand, q_len, heads, dim, stride, float(scale or 0.0), _dtype_code(q),
+        _ptr(out), _stream(stream)), name)
     return out
 
 

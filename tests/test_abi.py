@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 9
+    assert len(names) == 11
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -95,6 +95,30 @@ def test_attention_argument_errors(lib):
     assert call(R=0) == _lib.INVALID_ARGUMENT
     assert call(out=FAKE[0]) == _lib.INVALID_ARGUMENT      # out aliases q
     assert call(N=0) == _lib.OK
+
+
+def test_mapped_entry_points_argument_errors(lib):
+    def lin(**kw):
+        a = dict(x_req=FAKE[0], k_req=8, x_cand=FAKE[1], x_add=None, k_cand=8, w_req=FAKE[2],
+                 w_cand=FAKE[3], bias=None, ids=FAKE[4], R=2, N=16, D=8, dtype=1, act=1,
+                 out=FAKE[5], ws=FAKE[6], ws_bytes=1 << 20, stream=None)
+        a.update(kw)
+        return lib.rocs_ikbo_linear_mapped(*a.values())
+    assert lin(ids=None) == _lib.INVALID_ARGUMENT
+    assert b"cand_request_ids" in lib.rocs_last_error_message()
+    assert lin(ws_bytes=16) == _lib.WORKSPACE_TOO_SMALL
+    assert lin(out=P(0x50000 + 4)) == _lib.INVALID_ARGUMENT     # out overlaps the map
+    assert lin(k_req=0, x_req=None, w_req=None, ids=None, ws=None, ws_bytes=0, N=0) == _lib.OK
+
+    def att(**kw):
+        a = dict(q=FAKE[0], k=FAKE[1], v=FAKE[2], ids=FAKE[3], ko=FAKE[4], R=2, N=4, T=1, H=2,
+                 d=64, stride=0, scale=0.0, dtype=1, out=FAKE[5], stream=None)
+        a.update(kw)
+        return lib.rocs_dca_attention_mapped(*a.values())
+    assert att(ids=None) == _lib.INVALID_ARGUMENT
+    assert att(ko=None) == _lib.INVALID_ARGUMENT
+    assert att(T=0) == _lib.INVALID_ARGUMENT
+    assert att(N=0) == _lib.OK
 
 
 def test_interaction_argument_errors(lib):

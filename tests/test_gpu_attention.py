@@ -36,7 +36,7 @@ def _want(case, scale=None):
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"n{sum(s[0])}-L{sum(s[1])}")
 @pytest.mark.parametrize("head_dim", [64, 128])
-@pytest.mark.parametrize("q_len", [1, 3])
+@pytest.mark.parametrize("q_len", [1, 3, 32, 64])
 def test_attention_parity(gpu_lib, shape, head_dim, q_len):
     counts, lens = shape
     case = wl.attention_case(counts, lens, 2, head_dim, q_len=q_len, seed=head_dim + q_len)
@@ -115,3 +115,33 @@ def test_deterministic_and_candidate_isolation(gpu_lib):
     b = _attn(case)
     keep = np.arange(a.shape[0]) != 7
     np.testing.assert_array_equal(a[keep], b[keep])
+
+
+def test_mapped_attention_parity(gpu_lib):
+    # rocs_dca_attention_mapped: candidates shuffled so each request's are
+    # scattered; an empty history and a 1-key history included.
+    for head_dim, bf16 in ((128, True), (64, True), (64, False)):
+        case = wl.attention_case([37, 0, 90, 5, 21], [70, 5, 0, 129, 1], 2, head_dim, q_len=2,
+                                 seed=40 + head_dim, bf16=bf16)
+        perm = np.random.default_rng(head_dim).permutation(case.q.shape[0])
+        q = np.ascontiguousarray(case.q[perm])
+        m = ikbo.request_ids(case.cand_offsets)[perm]
+        dev = dev_bf16 if bf16 else dev_f32
+        got = host(ops.dca_attention_mapped(dev(q), dev(case.k), dev(case.v), dev_i32(m),
+                                            dev_i32(case.kv_offsets)))
+        want = ikbo.dca_attention(q, case.k, case.v, None, case.kv_offsets, request_map=m)
+        assert_close(got, round_bf16(want) if bf16 else want, f"mapped d{head_dim} bf16={bf16}")
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
+@pytest.mark.parametrize("q_len", [1, 32])
+def test_request_side_attention(gpu_lib, head_dim, q_len):
+    # A^R = Attn(Q^R, K, V): each request's own queries over its history
+    # (Eq. dca-attention), run as the identity map on the tiled kernel.
+    lens = [300, 0, 64, 1, 1000]
+    case = wl.attention_case([1] * len(lens), lens, 4, head_dim, q_len=q_len, seed=50 + q_len)
+    got = host(ops.dca_request_attention(dev_bf16(case.q), dev_bf16(case.k), dev_bf16(case.v),
+                                         dev_i32(case.kv_offsets)))
+    want = ikbo.dca_attention(case.q, case.k, case.v, np.arange(len(lens) + 1),
+                              case.kv_offsets)
+    assert_close(got, round_bf16(want), f"request-side d{head_dim} T{q_len}")

@@ -111,3 +111,51 @@ def test_empty_batch_is_noop(gpu_lib):
                         w_req=dev_bf16(np.zeros((8, 8), np.float32)),
                         cand_offsets=dev_i32([0, 0, 0]), out=out)
     assert out.numel() == 0
+
+
+# Per-candidate index map (rocs_ikbo_linear_mapped): the CSR cases with the
+# candidates shuffled, so one request's candidates are scattered over tiles.
+MAPPED = [
+    ([300, 0, 1, 211, 17], 96, 64, 160),
+    ([20000, 13000, 17001], 256, 128, 516),
+]
+
+
+def _dev(a, bf16):
+    return dev_bf16(a) if bf16 else dev_f32(a)
+
+
+@pytest.mark.parametrize("shape", MAPPED, ids=lambda s: f"R{len(s[0])}-N{sum(s[0])}-d{s[3]}")
+@pytest.mark.parametrize("bf16", [True, False], ids=["bf16", "fp32"])
+def test_mapped_linear_parity(gpu_lib, shape, bf16):
+    counts, kr, kc, d = shape
+    if not bf16 and sum(counts) > 1000:
+        counts = [c // 50 for c in counts]
+    case = wl.linear_case(counts, kr, kc, d, seed=31 + d, bf16=bf16, bias_std=0.3)
+    perm = np.random.default_rng(d).permutation(case.x_cand.shape[0])
+    xc = np.ascontiguousarray(case.x_cand[perm])
+    m = ikbo.request_ids(case.cand_offsets)[perm]
+    got = host(ops.ikbo_linear_mapped(
+        _dev(xc, bf16), _dev(case.w_cand, bf16), x_req=_dev(case.x_req, bf16),
+        w_req=_dev(case.w_req, bf16), cand_request_ids=dev_i32(m), bias=dev_f32(case.bias),
+        activation="relu"))
+    want = ikbo.ikbo_linear(case.x_req, xc, case.w_req, case.w_cand, case.bias, None, "relu",
+                            request_map=m)
+    assert_close(got, round_bf16(want) if bf16 else want, f"mapped {shape} bf16={bf16}")
+
+
+def test_mapped_index_probe_and_clamp(gpu_lib):
+    # Output 0 is the request index (x_req[r] = r, W_CR = e_0, W_CC = 0), so
+    # the device's map handling is checked bit-exactly. Ids outside [0, R) are
+    # clamped into range: -3 and R + 40 both read request R - 1.
+    r = 6
+    m = np.array([5, 0, 3, 3, 1, 5, -3, r + 40, 2, 0] * 40, dtype=np.int32)
+    n = m.size
+    x_req = np.repeat(np.arange(r, dtype=np.float32)[:, None], 16, axis=1)
+    w_req = np.zeros((8, 16), np.float32); w_req[0, 0] = 1.0
+    for dtype in (dev_bf16, dev_f32):
+        out = ops.ikbo_linear_mapped(dtype(np.ones((n, 8), np.float32)),
+                                     dtype(np.zeros((8, 8), np.float32)),
+                                     x_req=dtype(x_req), w_req=dtype(w_req),
+                                     cand_request_ids=dev_i32(m))
+        np.testing.assert_array_equal(host(out)[:, 0], np.clip(m, 0, r - 1) + (m < 0) * (r - 1))

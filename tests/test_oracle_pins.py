@@ -77,11 +77,11 @@ def test_offsets_validation(bad):
 # IKBO linear (Eq. glm-linear, Section 4.1, Eq. broadcast_add)
 # ---------------------------------------------------------------------------
 
-def _brute_linear(x_req, x_cand, w_req, w_cand, bias, off, act):
+def _brute_linear(x_req, x_cand, w_req, w_cand, bias, off, act, m=None):
     n_cand, d_out = x_cand.shape[0], w_cand.shape[0]
     out = np.zeros((n_cand, d_out))
     for n in range(n_cand):
-        r = max(i for i in range(len(off) - 1) if off[i] <= n)
+        r = m[n] if m is not None else max(i for i in range(len(off) - 1) if off[i] <= n)
         for d in range(d_out):
             acc = 0.0 if bias is None else float(bias[d])
             for k in range(x_req.shape[1]):
@@ -149,6 +149,38 @@ def test_ikbo_linear_glm_invariant_and_rows():
         ikbo.ikbo_linear(x_req, x_cand, w_req, w_cand, None, off, "relu", rows=rows), base[rows])
 
 
+@pytest.mark.parametrize("act", ["none", "relu"])
+def test_ikbo_linear_request_map_brute_force(act):
+    # Section 4.1's m as an arbitrary per-candidate map: requests interleaved,
+    # request 1 unused, request 3 used once.
+    rng = np.random.default_rng(21)
+    m = np.array([2, 0, 2, 3, 0, 0, 2])
+    x_req, x_cand = rng.standard_normal((4, 5)), rng.standard_normal((7, 3))
+    w_req, w_cand = rng.standard_normal((6, 5)), rng.standard_normal((6, 3))
+    bias = rng.standard_normal(6)
+    got = ikbo.ikbo_linear(x_req, x_cand, w_req, w_cand, bias, None, act, request_map=m)
+    want = _brute_linear(x_req, x_cand, w_req, w_cand, bias, None, act, m=m)
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
+
+
+def test_request_map_is_permutation_equivariant_and_checked():
+    # Reordering candidates together with their map entries reorders the
+    # output rows and changes nothing else; CSR offsets are the sorted case.
+    rng = np.random.default_rng(22)
+    counts = np.array([4, 0, 9, 2])
+    off = np.concatenate([[0], np.cumsum(counts)])
+    x_req, x_cand = rng.standard_normal((4, 6)), rng.standard_normal((15, 5))
+    w_req, w_cand = rng.standard_normal((3, 6)), rng.standard_normal((3, 5))
+    csr = ikbo.ikbo_linear(x_req, x_cand, w_req, w_cand, None, off, "relu")
+    perm = rng.permutation(15)
+    mapped = ikbo.ikbo_linear(x_req, x_cand[perm], w_req, w_cand, None, None, "relu",
+                              request_map=ikbo.request_ids(off)[perm])
+    np.testing.assert_array_equal(mapped, csr[perm])
+    for bad in ([0] * 14 + [4], [-1] + [0] * 14, [0] * 14):
+        with pytest.raises(ValueError):
+            ikbo.ikbo_linear(x_req, x_cand, w_req, w_cand, None, None, request_map=bad)
+
+
 def test_plain_linear_is_matmul():
     rng = np.random.default_rng(4)
     x, w, b = rng.standard_normal((8, 6)), rng.standard_normal((5, 6)), rng.standard_normal(5)
@@ -177,11 +209,11 @@ def test_projection_commutes_with_request_gather():
 # DCA attention (Eq. dca-attention)
 # ---------------------------------------------------------------------------
 
-def _brute_attention(q, k, v, cand_off, kv_off, scale):
+def _brute_attention(q, k, v, cand_off, kv_off, scale, m=None):
     n_cand, t_q, n_heads, d = q.shape
     out = np.zeros(q.shape)
     for n in range(n_cand):
-        r = max(i for i in range(len(cand_off) - 1) if cand_off[i] <= n)
+        r = m[n] if m is not None else max(i for i in range(len(cand_off) - 1) if cand_off[i] <= n)
         rows = range(kv_off[r], kv_off[r + 1])
         for t in range(t_q):
             for h in range(n_heads):
@@ -206,6 +238,33 @@ def test_attention_brute_force(mode):
     want = _brute_attention(q, k, v, cand_off, kv_off, 1 / math.sqrt(5))
     np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
     assert np.all(got[3:5] == 0.0)               # request 2 has an empty history
+
+
+@pytest.mark.parametrize("mode", ["explicit", "grouped"])
+def test_attention_request_map_brute_force(mode):
+    # Candidates of one request scattered through the batch (Section 4.3.1
+    # resolves m_i per candidate); request 2 has an empty history.
+    rng = np.random.default_rng(23)
+    m = np.array([1, 3, 0, 1, 2, 3, 1])
+    kv_off = np.array([0, 4, 9, 9, 11])
+    q = rng.standard_normal((7, 2, 3, 5)) * 2
+    k, v = rng.standard_normal((11, 3, 5)), rng.standard_normal((11, 3, 5))
+    got = ikbo.dca_attention(q, k, v, None, kv_off, mode=mode, chunk=2, request_map=m)
+    want = _brute_attention(q, k, v, None, kv_off, 1 / math.sqrt(5), m=m)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    assert np.all(got[4] == 0.0)
+
+
+def test_request_side_attention_is_the_identity_map():
+    # A^R = Attn(Q^R, K, V) (Eq. dca-attention): request r's own queries over
+    # r's own history, i.e. the candidate-side operator with m = identity.
+    rng = np.random.default_rng(24)
+    kv_off = np.array([0, 3, 3, 8])
+    q = rng.standard_normal((3, 4, 2, 6))
+    k, v = rng.standard_normal((8, 2, 6)), rng.standard_normal((8, 2, 6))
+    got = ikbo.dca_attention(q, k, v, np.arange(4), kv_off)
+    want = _brute_attention(q, k, v, None, kv_off, 1 / math.sqrt(6), m=np.arange(3))
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
 
 
 def test_attention_closed_forms():
