@@ -232,6 +232,58 @@ int32_t rocs_glm_interaction(const void* x_req, const void* x_cand,
 
 /*
  * ---------------------------------------------------------------------------
+ * rocs_ikbo_lcb: the two-group GLM linear compression block (Eq. glm-lcb,
+ * Eq. glm-lcb-two-groups): the field (row) axis of embedding matrices is
+ * mixed, block lower-triangularly.
+ *
+ *   y_req[r]  = W_RR X^R_r                      [o_req, emb]   once per request
+ *   y_cand[n] = W_CR X^R_{m_n} + W_CC X^C_n     [o_cand, emb]  per candidate
+ *
+ * IKBO form (Section 4.1, 4.2): one launch at batch size R forms y_req and
+ * Z_r = W_CR X^R_r (fp32, in the workspace) from the stacked weight
+ * [W_RR; W_CR]; the candidate kernel adds Z_{m_n} to W_CC X^C_n in its
+ * accumulators. No candidate-batched copy of X^R or Z is formed.
+ *
+ *   x_req   [R, f_req, emb_dim]       x_cand [N, f_cand, emb_dim]
+ *   w_rr    [o_req, f_req] (ignored when o_req == 0 or y_req is NULL)
+ *   w_cr    [o_cand, f_req]           w_cc   [o_cand, f_cand]
+ *   cand_offsets [R + 1]
+ *   y_req   [R, o_req, emb_dim] or NULL (request-side output skipped)
+ *   y_cand  [N, o_cand, emb_dim]
+ *   workspace  at least rocs_ikbo_lcb_workspace_size(R, o_cand, emb_dim) bytes,
+ *              256-byte aligned; scratch on return.
+ * No bias and no activation (the paper's LCB has neither); outputs do not
+ * overlap inputs, each other or the workspace.
+ *
+ * Fast path (bf16 MFMA candidate kernel): bf16, f_cand in {16, 32, 64}, and
+ * (emb_dim, o_cand) in {(128, 32), (64, 32), (64, 64)}, x_cand 16-byte and
+ * w_cc / y_cand 8-byte aligned. Other cases run a general kernel.
+ * ---------------------------------------------------------------------------
+ */
+size_t rocs_ikbo_lcb_workspace_size(int64_t num_requests, int64_t o_cand, int64_t emb_dim);
+
+int32_t rocs_ikbo_lcb(const void* x_req, const void* x_cand,
+                      const void* w_rr, const void* w_cr, const void* w_cc,
+                      const int32_t* cand_offsets, int64_t num_requests, int64_t num_cand,
+                      int32_t f_req, int32_t f_cand, int32_t o_req, int32_t o_cand,
+                      int32_t emb_dim, int32_t dtype, void* y_req, void* y_cand,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * rocs_ikbo_lcb_mapped: rocs_ikbo_lcb with m given as a per-candidate request
+ * id (cand_request_ids [N] int32, each in [0, R); an id outside the range is
+ * clamped into it, never read out of bounds). Same kernels, same fast path.
+ */
+int32_t rocs_ikbo_lcb_mapped(const void* x_req, const void* x_cand,
+                             const void* w_rr, const void* w_cr, const void* w_cc,
+                             const int32_t* cand_request_ids, int64_t num_requests,
+                             int64_t num_cand, int32_t f_req, int32_t f_cand, int32_t o_req,
+                             int32_t o_cand, int32_t emb_dim, int32_t dtype, void* y_req,
+                             void* y_cand, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * Index-map helpers (Section 4.1, m in {0..B_r-1}^{B_c}).
  *
  * rocs_request_ids: out_ids[n] = m_n for n < N, computed on the device by the

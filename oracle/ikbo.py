@@ -27,7 +27,7 @@ __all__ = [
     "request_ids", "check_offsets", "resolve_map", "activation",
     "ikbo_linear", "ikbo_linear_decomposed", "linear",
     "sequence_projection", "dca_attention",
-    "glm_fm", "glm_fm_masked_blocks", "amortized_flops",
+    "glm_fm", "glm_fm_masked_blocks", "glm_lcb", "glm_lcb_decomposed", "amortized_flops",
 ]
 
 _CHUNK = 16384
@@ -252,6 +252,65 @@ def dca_attention(q, k, v, cand_offsets, kv_offsets, scale=None,
                 o = _softmax_rows(s) @ vr[:, h, :]
                 out[order[g], :, h, :] = o.reshape(g.size, t_q, d)
     return out
+
+
+# ---------------------------------------------------------------------------
+# GLM linear compression block (Eq. glm-lcb, two-group form Eq. glm-lcb-two-groups).
+# ---------------------------------------------------------------------------
+
+def _lcb_full_weight(w_rr, w_cr, w_cc):
+    """[[W_RR, 0], [W_CR, W_CC]]: the block lower-triangular (GLM-masked) weight
+    over the stacked field axis [request fields; candidate fields]."""
+    o_r = 0 if w_rr is None else w_rr.shape[0]
+    f_r, f_c = w_cr.shape[1], w_cc.shape[1]
+    top = np.concatenate([np.zeros((0, f_r)) if w_rr is None else _f64(w_rr),
+                          np.zeros((o_r, f_c))], axis=1)           # W_RC masked to 0
+    bottom = np.concatenate([_f64(w_cr), _f64(w_cc)], axis=1)
+    return np.concatenate([top, bottom], axis=0), o_r
+
+
+def glm_lcb(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets, request_map=None, rows=None,
+            chunk=4096):
+    """Both outputs of a two-group LCB, by explicit broadcast (Eq. glm-lcb-two-groups).
+
+    X^R_r [F_r, E] and X^C_n [F_c, E] are field x embedding matrices. For each
+    candidate n the owning request's X^R_{m_n} is copied and stacked on top of
+    X^C_n, and the masked block weight [[W_RR, 0], [W_CR, W_CC]] is applied
+    to the stacked field axis; the candidate rows of the result are y_cand[n].
+    The request rows are y_req[r], taken per request with the candidate part
+    zero (the masked block makes them independent of it).
+
+    x_req [R, F_r, E], x_cand [N, F_c, E], w_rr [O_r, F_r] or None,
+    w_cr [O_c, F_r], w_cc [O_c, F_c]. Returns float64 (y_req [R, O_r, E] or
+    None, y_cand [N, O_c, E] or [len(rows), O_c, E]).
+    """
+    x_req = _f64(x_req)
+    x_cand = np.asarray(x_cand)
+    n_req, f_r, e = x_req.shape
+    n_cand, f_c, _ = x_cand.shape
+    w_full, o_r = _lcb_full_weight(w_rr, w_cr, w_cc)
+    m = resolve_map(cand_offsets, request_map, n_cand, n_req)
+    y_req = None
+    if w_rr is not None:
+        stacked = np.concatenate([x_req, np.zeros((n_req, f_c, e))], axis=1)
+        y_req = (w_full @ stacked)[:, :o_r]
+    sel = np.arange(n_cand) if rows is None else np.asarray(rows, dtype=np.int64)
+    y_cand = np.empty((sel.size, w_full.shape[0] - o_r, e))
+    for s0 in range(0, sel.size, chunk):
+        idx = sel[s0:s0 + chunk]
+        stacked = np.concatenate([x_req[m[idx]], _f64(x_cand[idx])], axis=1)   # broadcast copy
+        y_cand[s0:s0 + chunk] = (w_full @ stacked)[:, o_r:]
+    return y_req, y_cand
+
+
+def glm_lcb_decomposed(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets):
+    """The same outputs by the Section 4.1 decomposition (used only as a pin):
+    Z_r = W_CR X^R_r at batch size B_r, then Y^C_n = Z_{m_n} + W_CC X^C_n."""
+    m = request_ids(check_offsets(cand_offsets, np.asarray(x_cand).shape[0]))
+    z = _f64(w_cr) @ _f64(x_req)                              # [R, O_c, E]
+    y_cand = _f64(w_cc) @ _f64(x_cand) + z[m]
+    y_req = None if w_rr is None else _f64(w_rr) @ _f64(x_req)
+    return y_req, y_cand
 
 
 # ---------------------------------------------------------------------------

@@ -307,6 +307,104 @@ int32_t rocs_glm_interaction(const void* x_req, const void* x_cand, const int32_
   return ok();
 }
 
+size_t rocs_ikbo_lcb_workspace_size(int64_t num_requests, int64_t o_cand, int64_t emb_dim) {
+  if (num_requests <= 0 || o_cand <= 0 || emb_dim <= 0) return 0;
+  return align256((size_t)num_requests * (size_t)o_cand * (size_t)emb_dim * sizeof(float));
+}
+
+}  // extern "C"
+
+namespace {
+
+int32_t lcb_impl(const char* name, bool mapped, const void* x_req, const void* x_cand,
+                 const void* w_rr, const void* w_cr, const void* w_cc,
+                 const int32_t* cand_offsets, const int32_t* cand_ids, int64_t R, int64_t N,
+                 int32_t f_req, int32_t f_cand, int32_t o_req, int32_t o_cand, int32_t emb,
+                 int32_t dtype, void* y_req, void* y_cand, void* workspace,
+                 size_t workspace_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (R < 0 || N < 0 || f_req < 1 || f_cand < 1 || o_req < 0 || o_cand < 1 || emb < 1)
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "need R >= 0, N >= 0, f_req >= 1, f_cand >= 1, o_req >= 0, o_cand >= 1, "
+                "emb_dim >= 1");
+  if (R > kMaxI32 || N > kMaxI32 || (int64_t)f_cand * emb > (1 << 24) ||
+      (int64_t)f_req * emb > (1 << 24) || (int64_t)(o_req + o_cand) * emb > (1 << 24))
+    return fail(ROCS_ERR_UNSUPPORTED, "size too large");
+  if (y_req == nullptr) o_req = 0;
+  // One thread per output element in the request kernel (and the general
+  // candidate kernel): keep both grids below 2^31 workgroups.
+  if (R * (int64_t)(o_req + o_cand) * emb / 256 >= kMaxI32 ||
+      N * (int64_t)o_cand * emb / 256 >= kMaxI32)
+    return fail(ROCS_ERR_UNSUPPORTED, "batch too large");
+  if (R == 0) {
+    if (N > 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests");
+    return ok();
+  }
+  if (x_req == nullptr || w_cr == nullptr || (o_req > 0 && w_rr == nullptr) ||
+      (N > 0 && (x_cand == nullptr || w_cc == nullptr || y_cand == nullptr ||
+                 (mapped ? cand_ids == nullptr : cand_offsets == nullptr))))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
+  const size_t need = rocs_ikbo_lcb_workspace_size(R, o_cand, emb);
+  if (workspace == nullptr || workspace_bytes < need)
+    return fail(ROCS_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned(workspace, 256))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  const size_t es = esize(dtype);
+  const size_t yr_bytes = (size_t)R * o_req * emb * es, yc_bytes = (size_t)N * o_cand * emb * es;
+  const struct { const void* p; size_t n; } ins[] = {
+      {x_req, (size_t)R * f_req * emb * es}, {x_cand, (size_t)N * f_cand * emb * es},
+      {w_rr, (size_t)o_req * f_req * es}, {w_cr, (size_t)o_cand * f_req * es},
+      {w_cc, (size_t)o_cand * f_cand * es}, {cand_offsets, (size_t)(R + 1) * 4},
+      {cand_ids, (size_t)N * 4}};
+  for (const auto& in : ins)
+    if (overlap(y_req, yr_bytes, in.p, in.n) || overlap(y_cand, yc_bytes, in.p, in.n) ||
+        overlap(workspace, need, in.p, in.n))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "an output or the workspace overlaps an input");
+  if (overlap(y_req, yr_bytes, y_cand, yc_bytes) || overlap(y_req, yr_bytes, workspace, need) ||
+      overlap(y_cand, yc_bytes, workspace, need))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "outputs and workspace overlap");
+
+  rocs::LcbArgs a{};
+  a.x_req = x_req; a.x_cand = x_cand; a.w_rr = w_rr; a.w_cr = w_cr; a.w_cc = w_cc;
+  a.cand_offsets = mapped ? nullptr : cand_offsets;
+  a.ids = mapped ? cand_ids : nullptr;
+  a.R = R; a.N = N; a.f_req = f_req; a.f_cand = f_cand; a.o_req = o_req; a.o_cand = o_cand;
+  a.emb = emb; a.bf16 = dtype == ROCS_DTYPE_BF16;
+  a.y_req = o_req > 0 ? y_req : nullptr; a.y_cand = y_cand;
+  a.z = static_cast<float*>(workspace);
+  const bool fast = a.bf16 && rocs::lcb_fast_shape(f_cand, o_cand, emb) && aligned(x_cand, 16) &&
+                    aligned(w_cc, 8) && aligned(y_cand, 8);
+  const hipError_t e = rocs::launch_lcb(a, fast, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rocs_ikbo_lcb(const void* x_req, const void* x_cand, const void* w_rr, const void* w_cr,
+                      const void* w_cc, const int32_t* cand_offsets, int64_t R, int64_t N,
+                      int32_t f_req, int32_t f_cand, int32_t o_req, int32_t o_cand,
+                      int32_t emb_dim, int32_t dtype, void* y_req, void* y_cand,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  return lcb_impl("rocs_ikbo_lcb", false, x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets,
+                  nullptr, R, N, f_req, f_cand, o_req, o_cand, emb_dim, dtype, y_req, y_cand,
+                  workspace, workspace_bytes, stream);
+}
+
+int32_t rocs_ikbo_lcb_mapped(const void* x_req, const void* x_cand, const void* w_rr,
+                             const void* w_cr, const void* w_cc,
+                             const int32_t* cand_request_ids, int64_t R, int64_t N,
+                             int32_t f_req, int32_t f_cand, int32_t o_req, int32_t o_cand,
+                             int32_t emb_dim, int32_t dtype, void* y_req, void* y_cand,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return lcb_impl("rocs_ikbo_lcb_mapped", true, x_req, x_cand, w_rr, w_cr, w_cc, nullptr,
+                  cand_request_ids, R, N, f_req, f_cand, o_req, o_cand, emb_dim, dtype, y_req,
+                  y_cand, workspace, workspace_bytes, stream);
+}
+
 int32_t rocs_request_ids(const int32_t* cand_offsets, int64_t R, int64_t N, int32_t* out_ids,
                          void* stream) {
   if (R < 0 || N < 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "negative size");

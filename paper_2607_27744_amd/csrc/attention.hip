@@ -76,16 +76,6 @@ constexpr float kWeightBound = 0x1p64f;
 // ---------------------------------------------------------------------------
 constexpr int kStages = 4;       // K/V ring depth in LDS (loads run two stages ahead)
 
-// 16-byte chunk c of history row `key` (D bf16 = 2D bytes) sits at chunk
-// position c ^ kv_swizzle(key) of its LDS row. Conflict-free for both read
-// patterns: 16 consecutive rows at one chunk (K fragments) and 4 consecutive
-// rows x 4 consecutive chunks (transposing V reads).
-template <int D>
-__device__ __forceinline__ int kv_swizzle(int key) {
-  if constexpr (D == 128) return ((key & 3) << 2) | ((key >> 2) & 3);
-  else return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
-}
-
 template <int D> constexpr int attn_waves() { return D == 64 ? 4 : 8; }
 
 template <int D, int W>

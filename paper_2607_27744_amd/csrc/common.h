@@ -181,6 +181,19 @@ __device__ __forceinline__ void lds_dma16_sv(const void* sbase, uint32_t voff, u
                :: "v"(voff), "s"(sbase), "s"(dst) : "m0");
 }
 
+// LDS row swizzle for rows of D bf16 (2D bytes, D = 64 or 128) staged in
+// their global layout: 16-byte chunk c of row `key` sits at chunk position
+// c ^ kv_swizzle(key). Conflict-free for both read patterns: 16 consecutive
+// rows at one chunk (row-major MFMA fragments) and 4 consecutive rows x 4
+// consecutive chunks (transposing reads). Depends on key bits 0-3 only, so
+// moving 16 rows keeps it, and chunk steps of 4 are an XOR of the offset.
+template <int D>
+__device__ __forceinline__ int kv_swizzle(int key) {
+  static_assert(D == 64 || D == 128, "row width");
+  if constexpr (D == 128) return ((key & 3) << 2) | ((key >> 2) & 3);
+  else return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
+}
+
 // Workgroup barrier for the LDS ring. Each wave has waited for its own DMA
 // loads before it arrives; the empty asm statements keep the compiler from
 // moving LDS accesses across the barrier.

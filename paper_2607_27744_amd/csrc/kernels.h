@@ -48,11 +48,29 @@ struct InteractionArgs {
   void* y_cand;
 };
 
+struct LcbArgs {
+  const void* x_req;    // [R, f_req, emb]
+  const void* x_cand;   // [N, f_cand, emb]
+  const void* w_rr;     // [o_req, f_req] (may be NULL when o_req == 0)
+  const void* w_cr;     // [o_cand, f_req]
+  const void* w_cc;     // [o_cand, f_cand]
+  const int32_t* cand_offsets;   // CSR [R + 1], or NULL with ids
+  const int32_t* ids;            // caller's per-candidate map, or NULL
+  int64_t R, N;
+  int f_req, f_cand, o_req, o_cand, emb;
+  bool bf16;
+  void* y_req;          // [R, o_req, emb] or NULL
+  void* y_cand;         // [N, o_cand, emb]
+  float* z;             // [R, o_cand, emb] workspace
+};
+
 // Each returns hipSuccess or the launch error.
 hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t* ids,
                               hipStream_t s);
 hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s);
 hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s);
 hipError_t launch_interaction(const InteractionArgs& a, bool fast, hipStream_t s);
+hipError_t launch_lcb(const LcbArgs& a, bool fast, hipStream_t s);
+bool lcb_fast_shape(int f_cand, int o_cand, int emb);
 
 }  // namespace rocs

@@ -16,7 +16,7 @@ from . import _lib
 __all__ = [
     "load_library", "ikbo_linear", "ikbo_linear_mapped", "linear_workspace_size",
     "dca_attention", "dca_attention_mapped", "dca_request_attention", "glm_interaction",
-    "request_ids", "validate_offsets", "RocsError",
+    "ikbo_lcb", "ikbo_lcb_mapped", "request_ids", "validate_offsets", "RocsError",
 ]
 
 RocsError = _lib.RocsError
@@ -228,6 +228,65 @@ def glm_interaction(x_req, x_cand, cand_offsets, *, request_side=True, candidate
         _dtype_code(x_req), _ptr(y_req if request_side else None),
         _ptr(y_cand if candidate_side else None), _stream(stream)), "rocs_glm_interaction")
     return (y_req if request_side else None), (y_cand if candidate_side else None)
+
+
+def ikbo_lcb(x_req, x_cand, w_cr, w_cc, cand_offsets, *, w_rr=None, y_req=None, y_cand=None,
+             workspace=None, stream=None):
+    """Two-group GLM LCB (Eq. glm-lcb-two-groups): returns (y_req [R, O_r, E] or None,
+    y_cand [N, O_c, E]); y_req = W_RR X^R when w_rr is given, y_cand = W_CR X^R_m + W_CC X^C.
+    x_req [R, F_r, E], x_cand [N, F_c, E], w_rr [O_r, F_r], w_cr [O_c, F_r], w_cc [O_c, F_c]."""
+    return _lcb(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets, None, y_req, y_cand, workspace,
+                stream)
+
+
+def ikbo_lcb_mapped(x_req, x_cand, w_cr, w_cc, cand_request_ids, *, w_rr=None, y_req=None,
+                    y_cand=None, workspace=None, stream=None):
+    """rocs_ikbo_lcb_mapped: ikbo_lcb with m given per candidate (int32 [N] in [0, R))."""
+    return _lcb(x_req, x_cand, w_rr, w_cr, w_cc, None, cand_request_ids, y_req, y_cand,
+                workspace, stream)
+
+
+def _lcb(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets, cand_ids, y_req, y_cand, workspace,
+         stream):
+    lib = _lib.load()
+    mapped = cand_ids is not None
+    _need(x_req.dim() == 3 and x_cand.dim() == 3, "x_req / x_cand must be [rows, fields, emb]")
+    n_req, f_req, emb = x_req.shape
+    n_cand, f_cand, emb_c = x_cand.shape
+    _need(emb == emb_c, "embedding widths differ")
+    o_cand = w_cc.shape[0]
+    _need(w_cc.shape == (o_cand, f_cand) and w_cr.shape == (o_cand, f_req),
+          "w_cc must be [O_c, F_c] and w_cr [O_c, F_r]")
+    o_req = 0 if w_rr is None else w_rr.shape[0]
+    _need(w_rr is None or w_rr.shape == (o_req, f_req), "w_rr must be [O_r, F_r]")
+    for t in (x_cand, w_rr, w_cr, w_cc):
+        _need(t is None or t.dtype == x_req.dtype, "inputs must share one dtype")
+    for t in (x_req, x_cand, w_rr, w_cr, w_cc):
+        _need(t is None or t.is_contiguous(), "tensors must be contiguous")
+    if mapped:
+        _request_map(cand_ids, n_cand)
+    else:
+        _offsets(cand_offsets, n_req)
+    if o_req > 0 and y_req is None:
+        y_req = torch.empty((n_req, o_req, emb), dtype=x_req.dtype, device=x_req.device)
+    if y_cand is None:
+        y_cand = torch.empty((n_cand, o_cand, emb), dtype=x_req.dtype, device=x_req.device)
+    _need(y_cand.shape == (n_cand, o_cand, emb) and y_cand.dtype == x_req.dtype and
+          y_cand.is_contiguous(), "y_cand must be a contiguous [N, O_c, E] tensor")
+    _need(y_req is None or (y_req.shape == (n_req, o_req, emb) and y_req.dtype == x_req.dtype
+                            and y_req.is_contiguous()), "y_req must be [R, O_r, E]")
+    need = int(lib.rocs_ikbo_lcb_workspace_size(n_req, o_cand, emb))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x_req.device)
+    _on_gpu(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets, cand_ids, y_req, y_cand, workspace)
+    fn, name = ((lib.rocs_ikbo_lcb_mapped, "rocs_ikbo_lcb_mapped") if mapped
+                else (lib.rocs_ikbo_lcb, "rocs_ikbo_lcb"))
+    _lib.check(fn(
+        _ptr(x_req), _ptr(x_cand), _ptr(w_rr), _ptr(w_cr), _ptr(w_cc),
+        _ptr(cand_ids if mapped else cand_offsets), n_req, n_cand, f_req, f_cand, o_req, o_cand,
+        emb, _dtype_code(x_req), _ptr(y_req), _ptr(y_cand), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)), name)
+    return y_req, y_cand
 
 
 def request_ids(cand_offsets, num_cand, *, stream=None):

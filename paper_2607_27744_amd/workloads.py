@@ -37,7 +37,7 @@ import torch
 
 __all__ = [
     "tensor_rng", "normal", "offsets_from_counts", "linear_case",
-    "attention_case", "fm_case", "make_workload", "WORKLOAD_NAMES",
+    "attention_case", "fm_case", "lcb_case", "make_workload", "WORKLOAD_NAMES",
 ]
 
 WORKLOAD_NAMES = {
@@ -136,6 +136,26 @@ def fm_case(counts, f_req, f_cand, emb_dim, *, seed=0, config_id=300, bf16=True)
                       bf16=bf16),
         n_req=counts.size, n_cand=int(counts.sum()), f_req=f_req, f_cand=f_cand,
         emb_dim=emb_dim,
+    )
+
+
+def lcb_case(counts, f_req, f_cand, o_req, o_cand, emb_dim, *, seed=0, config_id=400,
+             bf16=True):
+    """One two-group LCB problem: x_req [R, F_r, E], x_cand [N, F_c, E], w_rr
+    [O_r, F_r] (None when O_r = 0) and [w_cr | w_cc] drawn as one [O_c, F_r +
+    F_c] matrix with std 1/sqrt(F_r + F_c)."""
+    counts = np.asarray(counts, dtype=np.int64)
+    n_req, n_cand = counts.size, int(counts.sum())
+    w = normal(tensor_rng(seed, config_id, 3), (o_cand, f_req + f_cand),
+               std=1.0 / np.sqrt(f_req + f_cand), bf16=bf16)
+    return SimpleNamespace(
+        cand_offsets=offsets_from_counts(counts),
+        x_req=normal(tensor_rng(seed, config_id, 1), (n_req, f_req, emb_dim), bf16=bf16),
+        x_cand=normal(tensor_rng(seed, config_id, 2), (n_cand, f_cand, emb_dim), bf16=bf16),
+        w_rr=(normal(tensor_rng(seed, config_id, 4), (o_req, f_req), std=1.0 / np.sqrt(f_req),
+                     bf16=bf16) if o_req else None),
+        w_cr=np.ascontiguousarray(w[:, :f_req]), w_cc=np.ascontiguousarray(w[:, f_req:]),
+        n_req=n_req, n_cand=n_cand,
     )
 
 

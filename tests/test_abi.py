@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 11
+    assert len(names) == 14
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -119,6 +119,28 @@ def test_mapped_entry_points_argument_errors(lib):
     assert att(ko=None) == _lib.INVALID_ARGUMENT
     assert att(T=0) == _lib.INVALID_ARGUMENT
     assert att(N=0) == _lib.OK
+
+
+def test_lcb_argument_errors(lib):
+    def call(fn=lib.rocs_ikbo_lcb, **kw):
+        a = dict(xr=FAKE[0], xc=FAKE[1], wrr=FAKE[2], wcr=FAKE[3], wcc=FAKE[4], co=FAKE[5], R=2,
+                 N=4, fr=16, fc=16, orq=32, oc=32, e=64, dtype=1, yr=FAKE[6], yc=FAKE[7],
+                 ws=FAKE[8], ws_bytes=1 << 20, stream=None)
+        a.update(kw)
+        return fn(*a.values())
+    assert lib.rocs_ikbo_lcb_workspace_size(2, 32, 64) == 2 * 32 * 64 * 4
+    assert lib.rocs_ikbo_lcb_workspace_size(0, 32, 64) == 0
+    assert call(dtype=5) == _lib.INVALID_ARGUMENT
+    assert call(fc=0) == _lib.INVALID_ARGUMENT
+    assert call(oc=0) == _lib.INVALID_ARGUMENT
+    assert call(wcr=None) == _lib.INVALID_ARGUMENT
+    assert call(co=None) == _lib.INVALID_ARGUMENT
+    assert call(fn=lib.rocs_ikbo_lcb_mapped, co=None, ws_bytes=64) == _lib.WORKSPACE_TOO_SMALL
+    assert call(ws_bytes=64) == _lib.WORKSPACE_TOO_SMALL
+    assert call(ws=P(0x90010)) == _lib.INVALID_ARGUMENT           # not 256-aligned
+    assert call(yc=FAKE[1]) == _lib.INVALID_ARGUMENT              # y_cand aliases x_cand
+    assert call(R=0) == _lib.INVALID_ARGUMENT                     # candidates without requests
+    assert call(R=0, N=0) == _lib.OK
 
 
 def test_interaction_argument_errors(lib):

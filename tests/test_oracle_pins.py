@@ -351,6 +351,82 @@ def test_attention_matches_torch_sdpa():
 
 
 # ---------------------------------------------------------------------------
+# GLM linear compression block (Eq. glm-lcb, glm-lcb-two-groups)
+# ---------------------------------------------------------------------------
+
+def test_lcb_brute_force():
+    rng = np.random.default_rng(31)
+    off = np.array([0, 2, 2, 5])
+    f_r, f_c, o_r, o_c, e = 3, 2, 4, 3, 5
+    x_req, x_cand = rng.standard_normal((3, f_r, e)), rng.standard_normal((5, f_c, e))
+    w_rr, w_cr, w_cc = (rng.standard_normal((o_r, f_r)), rng.standard_normal((o_c, f_r)),
+                        rng.standard_normal((o_c, f_c)))
+    y_req, y_cand = ikbo.glm_lcb(x_req, x_cand, w_rr, w_cr, w_cc, off, chunk=2)
+    for r in range(3):
+        for o in range(o_r):
+            for j in range(e):
+                want = sum(w_rr[o, f] * x_req[r, f, j] for f in range(f_r))
+                assert abs(y_req[r, o, j] - want) < 1e-12
+    for n in range(5):
+        r = max(i for i in range(3) if off[i] <= n)
+        for o in range(o_c):
+            for j in range(e):
+                want = (sum(w_cr[o, f] * x_req[r, f, j] for f in range(f_r)) +
+                        sum(w_cc[o, f] * x_cand[n, f, j] for f in range(f_c)))
+                assert abs(y_cand[n, o, j] - want) < 1e-12
+
+
+def test_lcb_equals_decomposition_exactly_and_is_glm_compliant():
+    # Integers: every partial sum is exact, so broadcast-then-compute and the
+    # Section 4.1 decomposition agree bit for bit.
+    rng = np.random.default_rng(32)
+    counts = np.array([3, 0, 6, 1])
+    off = np.concatenate([[0], np.cumsum(counts)])
+    ints = lambda *sh: rng.integers(-3, 4, size=sh).astype(np.float64)  # noqa: E731
+    x_req, x_cand = ints(4, 7, 6), ints(10, 5, 6)
+    w_rr, w_cr, w_cc = ints(2, 7), ints(3, 7), ints(3, 5)
+    a = ikbo.glm_lcb(x_req, x_cand, w_rr, w_cr, w_cc, off, chunk=3)
+    b = ikbo.glm_lcb_decomposed(x_req, x_cand, w_rr, w_cr, w_cc, off)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    # Eq. glm-invariant: a candidate change moves only its own row; the
+    # request-side output never depends on candidates.
+    x2 = x_cand.copy(); x2[4] += 5.0
+    c = ikbo.glm_lcb(x_req, x2, w_rr, w_cr, w_cc, off)
+    np.testing.assert_array_equal(c[0], a[0])
+    keep = np.arange(10) != 4
+    np.testing.assert_array_equal(c[1][keep], a[1][keep])
+    assert not np.array_equal(c[1][4], a[1][4])
+
+
+def test_lcb_special_cases_reduce_to_matmul():
+    # W_CR = 0: each candidate's output is the library product W_CC X^C_n.
+    rng = np.random.default_rng(33)
+    x_req, x_cand = rng.standard_normal((2, 4, 8)), rng.standard_normal((6, 3, 8))
+    w_cc = rng.standard_normal((5, 3))
+    _, y = ikbo.glm_lcb(x_req, x_cand, None, np.zeros((5, 4)), w_cc, [0, 2, 6])
+    want = torch.matmul(torch.from_numpy(w_cc), torch.from_numpy(x_cand)).numpy()
+    np.testing.assert_allclose(y, want, rtol=1e-13, atol=1e-13)
+    # W_CC = 0: every candidate of request r receives W_CR X^R_r.
+    w_cr = rng.standard_normal((5, 4))
+    _, y = ikbo.glm_lcb(x_req, x_cand, None, w_cr, np.zeros((5, 3)), [0, 2, 6])
+    zr = torch.matmul(torch.from_numpy(w_cr), torch.from_numpy(x_req)).numpy()
+    np.testing.assert_allclose(y, zr[[0, 0, 1, 1, 1, 1]], rtol=1e-13, atol=1e-13)
+
+
+def test_lcb_request_map_permutation():
+    rng = np.random.default_rng(34)
+    off = np.array([0, 4, 4, 9])
+    x_req, x_cand = rng.standard_normal((3, 5, 4)), rng.standard_normal((9, 2, 4))
+    w_cr, w_cc = rng.standard_normal((3, 5)), rng.standard_normal((3, 2))
+    _, base = ikbo.glm_lcb(x_req, x_cand, None, w_cr, w_cc, off)
+    perm = rng.permutation(9)
+    _, got = ikbo.glm_lcb(x_req, x_cand[perm], None, w_cr, w_cc, None,
+                          request_map=ikbo.request_ids(off)[perm])
+    np.testing.assert_array_equal(got, base[perm])
+
+
+# ---------------------------------------------------------------------------
 # GLM factorization machine (Eq. glm-fm, glm-fm-two-groups)
 # ---------------------------------------------------------------------------
 
