@@ -135,7 +135,8 @@ def test_lcb_argument_errors(lib):
     assert call(oc=0) == _lib.INVALID_ARGUMENT
     assert call(wcr=None) == _lib.INVALID_ARGUMENT
     assert call(co=None) == _lib.INVALID_ARGUMENT
-    assert call(fn=lib.rocs_ikbo_lcb_mapped, co=None, ws_bytes=64) == _lib.WORKSPACE_TOO_SMALL
+    assert call(fn=lib.rocs_ikbo_lcb_mapped, co=None) == _lib.INVALID_ARGUMENT   # null map
+    assert call(fn=lib.rocs_ikbo_lcb_mapped, ws_bytes=64) == _lib.WORKSPACE_TOO_SMALL
     assert call(ws_bytes=64) == _lib.WORKSPACE_TOO_SMALL
     assert call(ws=P(0x90010)) == _lib.INVALID_ARGUMENT           # not 256-aligned
     assert call(yc=FAKE[1]) == _lib.INVALID_ARGUMENT              # y_cand aliases x_cand
