@@ -116,6 +116,36 @@ int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req,
 
 /*
  * ---------------------------------------------------------------------------
+ * rocs_glm_linear: both outputs of a two-group GLM linear layer
+ * (Eq. glm-linear with K = 2):
+ *
+ *   y_req[r]  = act( W_RR x_req[r] + b_req )                      [R, d_req]
+ *   y_cand[n] = act( W_CR x_req[m_n] + W_CC xc[n] + b_cand )      [N, d_cand]
+ *
+ * (the masked block W_RC never exists). The request-side products W_RR x^R
+ * and W_CR x^R come from one GEMM at batch size R over the stacked weight
+ * [W_RR; W_CR] (Section 4.1); the candidate side is rocs_ikbo_linear.
+ *
+ *   w_rr [d_req, k_req], w_cr [d_cand, k_req], w_cc [d_cand, k_cand]
+ *   b_req [d_req] fp32 or NULL; b_cand [d_cand] fp32 or NULL
+ *   y_req [R, d_req] (required), y_cand [N, d_cand] (may be NULL iff N == 0)
+ *   k_req >= 1, d_req >= 1; every other argument, the workspace
+ *   (rocs_ikbo_linear_workspace_size(R, N, d_cand, k_req) bytes) and the
+ *   errors as for rocs_ikbo_linear. N == 0 still produces y_req.
+ * Fast path: that of rocs_ikbo_linear, plus d_req a multiple of 4, w_rr and
+ * b_req 16-byte and y_req 8-byte aligned.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_glm_linear(const void* x_req, int64_t k_req,
+                        const void* x_cand, const void* x_cand_add, int64_t k_cand,
+                        const void* w_rr, const void* w_cr, const void* w_cc,
+                        const float* b_req, const float* b_cand, const int32_t* cand_offsets,
+                        int64_t num_requests, int64_t num_cand, int64_t d_req, int64_t d_cand,
+                        int32_t dtype, int32_t activation, void* y_req, void* y_cand,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * rocs_ikbo_linear_mapped: rocs_ikbo_linear with the index map m given as a
  * per-candidate request id instead of CSR offsets (Section 4.1 defines m as
  * any map {0..B_c-1} -> {0..B_r-1}; candidates of one request need not be

@@ -25,7 +25,7 @@ import numpy as np
 
 __all__ = [
     "request_ids", "check_offsets", "resolve_map", "activation",
-    "ikbo_linear", "ikbo_linear_decomposed", "linear",
+    "ikbo_linear", "ikbo_linear_decomposed", "glm_linear", "linear",
     "sequence_projection", "dca_attention",
     "glm_fm", "glm_fm_masked_blocks", "glm_lcb", "glm_lcb_decomposed", "amortized_flops",
 ]
@@ -142,6 +142,32 @@ def ikbo_linear_decomposed(x_req, x_cand, w_req, w_cand, bias, cand_offsets,
     if bias is not None:
         pre = pre + _f64(bias)
     return activation(pre, act)
+
+
+def glm_linear(x_req, x_cand, w_rr, w_cr, w_cc, b_req, b_cand, cand_offsets, act="none"):
+    """Both outputs of a two-group GLM linear (Eq. glm-linear, K = 2), by explicit
+    broadcast with the masked block weight.
+
+    The full weight over the stacked input [x^R; x^C] is [[W_RR, 0], [W_CR, W_CC]]
+    (the block W_RC is masked to zero) and the bias is [b^R; b^C]. Every
+    candidate gets a copy of its request's x^R; the candidate rows of
+    act(W x + b) are y^C[n]. The request rows are y^R[r], taken per request
+    with the candidate part zero (the mask makes them independent of it).
+    Returns float64 (y_req [R, d_req], y_cand [N, d_cand]).
+    """
+    x_req, x_cand = _f64(x_req), _f64(x_cand)
+    w_rr, w_cr, w_cc = _f64(w_rr), _f64(w_cr), _f64(w_cc)
+    d_r, d_c = w_rr.shape[0], w_cc.shape[0]
+    k_r, k_c = x_req.shape[1], x_cand.shape[1]
+    w_full = np.block([[w_rr, np.zeros((d_r, k_c))], [w_cr, w_cc]])
+    b_full = np.concatenate([np.zeros(d_r) if b_req is None else _f64(b_req),
+                             np.zeros(d_c) if b_cand is None else _f64(b_cand)])
+    m = request_ids(check_offsets(cand_offsets, x_cand.shape[0]))
+    y_cand = activation(np.concatenate([x_req[m], x_cand], axis=1) @ w_full.T + b_full,
+                        act)[:, d_r:]
+    y_req = activation(np.concatenate([x_req, np.zeros((x_req.shape[0], k_c))], axis=1)
+                       @ w_full.T + b_full, act)[:, :d_r]
+    return y_req, y_cand
 
 
 def linear(x, w, bias=None, act="none", rows=None):

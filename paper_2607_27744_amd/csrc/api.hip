@@ -79,12 +79,21 @@ namespace {
 // Shared by rocs_ikbo_linear (CSR offsets) and rocs_ikbo_linear_mapped (a
 // per-candidate request map, `mapped`): only one of cand_offsets / cand_ids
 // is read.
+struct RequestSide {          // full GLM layer: Y^R = act(x_req W_RR^T + b^R)
+  const void* w_rr = nullptr;
+  const float* b_rr = nullptr;
+  void* y_req = nullptr;
+  int64_t d_req = 0;
+};
+
 int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_req,
                     const void* x_cand, const void* x_cand_add, int64_t k_cand,
                     const void* w_req, const void* w_cand, const float* bias,
                     const int32_t* cand_offsets, const int32_t* cand_ids, int64_t R, int64_t N,
                     int64_t d_out, int32_t dtype, int32_t activation, void* out,
-                    void* workspace, size_t workspace_bytes, void* stream) {
+                    void* workspace, size_t workspace_bytes, void* stream,
+                    const RequestSide& rs = RequestSide()) {
+  const bool full = rs.y_req != nullptr;
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (activation != ROCS_ACT_NONE && activation != ROCS_ACT_RELU)
     return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown activation %d", activation);
@@ -94,12 +103,20 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
                 "(got R=%lld N=%lld k_req=%lld k_cand=%lld d_out=%lld)",
                 (long long)R, (long long)N, (long long)k_req, (long long)k_cand,
                 (long long)d_out);
-  if (N > kMaxI32 || R > kMaxI32 || k_req > kMaxI32 || k_cand > kMaxI32 || d_out > kMaxI32)
+  if (N > kMaxI32 || R > kMaxI32 || k_req > kMaxI32 || k_cand > kMaxI32 || d_out > kMaxI32 ||
+      rs.d_req > kMaxI32)
     return fail(ROCS_ERR_UNSUPPORTED, "a size exceeds 2^31 - 1");
-  if (N == 0) return ok();
+  if (full) {
+    if (k_req < 1 || rs.d_req < 1 || rs.w_rr == nullptr || x_req == nullptr)
+      return fail(ROCS_ERR_INVALID_ARGUMENT,
+                  "the request-side output needs k_req >= 1, d_req >= 1, x_req and w_rr");
+    if (R == 0 && N == 0) return ok();
+  } else if (N == 0) {
+    return ok();
+  }
   if (k_req > 0 && R == 0)
     return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests to own them");
-  if (x_cand == nullptr || w_cand == nullptr || out == nullptr)
+  if (N > 0 && (x_cand == nullptr || w_cand == nullptr || out == nullptr))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "x_cand, w_cand and out must not be NULL");
   if (k_req > 0 && (x_req == nullptr || w_req == nullptr ||
                     (mapped ? cand_ids == nullptr : cand_offsets == nullptr)))
@@ -126,16 +143,27 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
       {cand_ids, (size_t)N * sizeof(int32_t), "cand_request_ids"},
       {need > 0 ? workspace : nullptr, need, "workspace"},
   };
-  for (const auto& in : ins)
+  const size_t yr_bytes = full ? (size_t)R * rs.d_req * es : 0;
+  for (const auto& in : ins) {
     if (overlap(out, out_bytes, in.p, in.n))
       return fail(ROCS_ERR_INVALID_ARGUMENT, "out overlaps %s", in.name);
+    if (overlap(rs.y_req, yr_bytes, in.p, in.n))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "y_req overlaps %s", in.name);
+  }
+  if (full && (overlap(rs.y_req, yr_bytes, out, out_bytes) ||
+               overlap(rs.y_req, yr_bytes, rs.w_rr, (size_t)rs.d_req * k_req * es) ||
+               overlap(rs.y_req, yr_bytes, rs.b_rr, (size_t)rs.d_req * sizeof(float)) ||
+               overlap(out, out_bytes, rs.w_rr, (size_t)rs.d_req * k_req * es) ||
+               overlap(out, out_bytes, rs.b_rr, (size_t)rs.d_req * sizeof(float))))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "y_req overlaps out or the W_RR / b^R inputs");
   if (need > 0) {
     const size_t zb = align256((size_t)R * d_out * sizeof(float));
     const struct { const void* p; size_t n; const char* name; } inw[] = {
         {x_req, (size_t)R * k_req * es, "x_req"}, {x_cand, (size_t)N * k_cand * es, "x_cand"},
         {w_req, (size_t)d_out * k_req * es, "w_req"}, {w_cand, (size_t)d_out * k_cand * es, "w_cand"},
         {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"},
-        {cand_ids, (size_t)N * sizeof(int32_t), "cand_request_ids"}};
+        {cand_ids, (size_t)N * sizeof(int32_t), "cand_request_ids"},
+        {rs.y_req, (size_t)R * rs.d_req * es, "y_req"}};
     for (const auto& in : inw)
       if (overlap(workspace, need, in.p, in.n))
         return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace overlaps %s", in.name);
@@ -149,6 +177,7 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
   a.bf16 = dtype == ROCS_DTYPE_BF16;
   a.relu = activation == ROCS_ACT_RELU;
   a.out = out;
+  a.w_rr = rs.w_rr; a.b_rr = rs.b_rr; a.y_req = rs.y_req; a.d_req = rs.d_req;
   if (need > 0) {
     a.z = static_cast<float*>(workspace);
     a.ids = mapped ? const_cast<int32_t*>(cand_ids)
@@ -159,7 +188,9 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
   const bool fast = a.bf16 && k_cand % 8 == 0 && k_req % 8 == 0 && d_out % 4 == 0 &&
                     aligned(x_cand, 16) && aligned(x_cand_add, 16) && aligned(w_cand, 16) &&
                     aligned(x_req, 16) && aligned(w_req, 16) && aligned(bias, 16) &&
-                    aligned(out, 16);
+                    aligned(out, 16) &&
+                    (!full || (rs.d_req % 4 == 0 && aligned(rs.w_rr, 16) &&
+                               aligned(rs.b_rr, 16) && aligned(rs.y_req, 8)));
   const hipError_t e = rocs::launch_linear(a, fast, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
   return ok();
@@ -177,6 +208,21 @@ int32_t rocs_ikbo_linear(const void* x_req, int64_t k_req, const void* x_cand,
   return linear_impl("rocs_ikbo_linear", false, x_req, k_req, x_cand, x_cand_add, k_cand,
                      w_req, w_cand, bias, cand_offsets, nullptr, R, N, d_out, dtype, activation,
                      out, workspace, workspace_bytes, stream);
+}
+
+int32_t rocs_glm_linear(const void* x_req, int64_t k_req, const void* x_cand,
+                        const void* x_cand_add, int64_t k_cand, const void* w_rr,
+                        const void* w_cr, const void* w_cc, const float* b_req,
+                        const float* b_cand, const int32_t* cand_offsets, int64_t R, int64_t N,
+                        int64_t d_req, int64_t d_cand, int32_t dtype, int32_t activation,
+                        void* y_req, void* y_cand, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  if (y_req == nullptr) return fail(ROCS_ERR_INVALID_ARGUMENT, "y_req must not be NULL");
+  RequestSide rs;
+  rs.w_rr = w_rr; rs.b_rr = b_req; rs.y_req = y_req; rs.d_req = d_req;
+  return linear_impl("rocs_glm_linear", false, x_req, k_req, x_cand, x_cand_add, k_cand, w_cr,
+                     w_cc, b_cand, cand_offsets, nullptr, R, N, d_cand, dtype, activation,
+                     y_cand, workspace, workspace_bytes, stream, rs);
 }
 
 int32_t rocs_ikbo_linear_mapped(const void* x_req, int64_t k_req, const void* x_cand,

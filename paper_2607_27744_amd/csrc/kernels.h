@@ -20,6 +20,11 @@ struct LinearArgs {
   float* z;          // [R, d_out] workspace (k_req > 0)
   int32_t* ids;      // [N] request of each candidate: workspace, or the caller's map
   bool ids_given;    // ids is the caller's map (no CSR offsets, no expansion)
+  // Full GLM layer: the request-side output Y^R = act(x_req W_RR^T + b^R).
+  const void* w_rr;  // [d_req, k_req]
+  const float* b_rr; // [d_req] or NULL
+  void* y_req;       // [R, d_req] or NULL (candidate output only)
+  int64_t d_req;
 };
 
 struct AttentionArgs {

@@ -29,17 +29,27 @@ __global__ __launch_bounds__(256) void request_ids_kernel(const int32_t* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Request-side GEMM, bf16 in, fp32 out: the request table Zb = X^R W_CR^T + b
-// (the bias is folded in here, once per request). One workgroup per 16 x 16
-// tile of Zb; its four waves split K in 32-wide steps (operands straight from
+// Request-side GEMM, bf16 in: the request table Zb = X^R W_CR^T + b (fp32;
+// the bias is folded in here, once per request) and, for a full GLM layer,
+// the request-side output Y^R = act(X^R W_RR^T + b^R) (bf16) from the same
+// launch: the stacked weight [W_RR; W_CR] of Section 4.1, one GEMM at batch
+// size R. One workgroup per 16 x 16 output tile (the W_RR column tiles come
+// first); its four waves split K in 32-wide steps (operands straight from
 // global memory into MFMA registers, each lane's 8 consecutive k are one
 // 16-byte load) and reduce through LDS in a fixed order. Workgroups past the
-// Zb tiles expand the index map when the candidate GEMM needs it.
+// tiles expand the index map when the candidate GEMM needs it.
 // ---------------------------------------------------------------------------
+struct RequestOut {          // the optional Y^R part of the stacked weight
+  const bf16_t* w;           // W_RR [d, K]
+  const float* bias;         // b^R [d] or NULL
+  bf16_t* y;                 // Y^R [R, d]
+  int d, tiles, relu;        // tiles = ceil(d / 16); 0 when there is no Y^R
+};
+
 __global__ __launch_bounds__(256) void request_gemm_bf16(
-    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w, const float* __restrict__ bias,
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w_in, const float* __restrict__ bias_in,
     float* __restrict__ z, const int32_t* __restrict__ off, int32_t* __restrict__ ids, int R,
-    int64_t N, int K, int D, int tiles_d, int z_blocks) {
+    int64_t N, int K, int D_in, int tiles_d, int z_blocks, RequestOut yr) {
   const int tid = threadIdx.x;
   if ((int)blockIdx.x >= z_blocks) {
     const int64_t n = (int64_t)(blockIdx.x - z_blocks) * 256 + tid;
@@ -48,7 +58,13 @@ __global__ __launch_bounds__(256) void request_gemm_bf16(
   }
   __shared__ f32x4 red[4][kWave];
   const int lane = tid & 63, wave = tid >> 6;
-  const int r0 = ((int)blockIdx.x / tiles_d) * 16, d0 = ((int)blockIdx.x % tiles_d) * 16;
+  const int tiles_all = yr.tiles + tiles_d;
+  const int t = (int)blockIdx.x % tiles_all;
+  const bool to_y = t < yr.tiles;                 // a column tile of Y^R
+  const bf16_t* w = to_y ? yr.w : w_in;
+  const float* bias = to_y ? yr.bias : bias_in;
+  const int D = to_y ? yr.d : D_in;
+  const int r0 = ((int)blockIdx.x / tiles_all) * 16, d0 = (to_y ? t : t - yr.tiles) * 16;
   const int row = lane & 15, kq = (lane >> 4) * 8;
   const bool dok = d0 + row < D, rok = r0 + row < R;
   const bf16_t* wp = w + (int64_t)(d0 + row) * K + kq;
@@ -68,7 +84,13 @@ __global__ __launch_bounds__(256) void request_gemm_bf16(
     const int d = d0 + (lane >> 4) * 4;
     if (rok && d < D) {
       if (bias != nullptr) s += *reinterpret_cast<const f32x4*>(bias + d);
-      *reinterpret_cast<f32x4*>(z + (int64_t)(r0 + row) * D + d) = s;
+      if (to_y) {
+        if (yr.relu) s = f32x4{fmaxf(s[0], 0.f), fmaxf(s[1], 0.f), fmaxf(s[2], 0.f), fmaxf(s[3], 0.f)};
+        *reinterpret_cast<u32x2*>(yr.y + (int64_t)(r0 + row) * D + d) =
+            u32x2{pack_bf16x2(s[0], s[1]), pack_bf16x2(s[2], s[3])};
+      } else {
+        *reinterpret_cast<f32x4*>(z + (int64_t)(r0 + row) * D + d) = s;
+      }
     }
   }
 }
@@ -708,7 +730,18 @@ hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t*
 }
 
 hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
-  if (!fast) return a.bf16 ? launch_generic<bf16_t>(a, s) : launch_generic<float>(a, s);
+  if (!fast) {
+    if (a.y_req != nullptr) {
+      // Y^R on the general path: the plain linear over the R request rows.
+      LinearArgs r{};
+      r.x_cand = a.x_req; r.w_cand = a.w_rr; r.bias = a.b_rr;
+      r.N = a.R; r.k_cand = a.k_req; r.d_out = a.d_req; r.R = 1;
+      r.bf16 = a.bf16; r.relu = a.relu; r.out = a.y_req;
+      const hipError_t e = a.bf16 ? launch_generic<bf16_t>(r, s) : launch_generic<float>(r, s);
+      if (e != hipSuccess || a.N == 0) return e;
+    }
+    return a.bf16 ? launch_generic<bf16_t>(a, s) : launch_generic<float>(a, s);
+  }
   // The streaming kernel needs request-aligned tiles, i.e. CSR offsets; a
   // caller's per-candidate map takes the kernel with per-row request lookup.
   const bool stream = !a.ids_given && a.x_cand_add == nullptr && a.k_cand % kStreamBK == 0 &&
@@ -716,16 +749,21 @@ hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
                       ((a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN) *
                               ((a.d_out + kStreamBM - 1) / kStreamBM) < (int64_t(1) << 31);
   if (a.k_req > 0) {
-    const int tiles_d = (int)((a.d_out + 15) / 16);
-    const int z_blocks = tiles_d * (int)((a.R + 15) / 16);
+    RequestOut yr{static_cast<const bf16_t*>(a.w_rr), a.b_rr, static_cast<bf16_t*>(a.y_req),
+                  (int)a.d_req, a.y_req != nullptr ? (int)((a.d_req + 15) / 16) : 0,
+                  (int)a.relu};
+    // No candidates: only the Y^R tiles (the request table has no reader).
+    const int tiles_d = a.N > 0 ? (int)((a.d_out + 15) / 16) : 0;
+    const int z_blocks = (yr.tiles + tiles_d) * (int)((a.R + 15) / 16);
     const int id_blocks = stream || a.ids_given ? 0 : (int)((a.N + 255) / 256);
     hipError_t e = launch_kernel(request_gemm_bf16, dim3(z_blocks + id_blocks), dim3(256), s,
                                  static_cast<const bf16_t*>(a.x_req),
                                  static_cast<const bf16_t*>(a.w_req), a.bias, a.z,
                                  a.cand_offsets, a.ids, (int)a.R, a.N, (int)a.k_req,
-                                 (int)a.d_out, tiles_d, z_blocks);
+                                 (int)a.d_out, tiles_d, z_blocks, yr);
     if (e != hipSuccess) return e;
   }
+  if (a.N == 0) return hipSuccess;      // request-side output only
   if (stream) {
     const int tiles_m = (int)((a.d_out + kStreamBM - 1) / kStreamBM);
     const int64_t slots = (a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN;

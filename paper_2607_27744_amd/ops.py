@@ -14,7 +14,7 @@ import torch
 from . import _lib
 
 __all__ = [
-    "load_library", "ikbo_linear", "ikbo_linear_mapped", "linear_workspace_size",
+    "load_library", "ikbo_linear", "ikbo_linear_mapped", "glm_linear", "linear_workspace_size",
     "dca_attention", "dca_attention_mapped", "dca_request_attention", "glm_interaction",
     "ikbo_lcb", "ikbo_lcb_mapped", "request_ids", "validate_offsets", "RocsError",
 ]
@@ -95,8 +95,32 @@ def ikbo_linear_mapped(x_cand, w_cand, *, x_req=None, w_req=None, cand_request_i
                    activation, x_cand_add, out, workspace, stream)
 
 
+def glm_linear(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets, *, b_req=None, b_cand=None,
+               activation="none", x_cand_add=None, y_req=None, y_cand=None, workspace=None,
+               stream=None):
+    """Both outputs of a two-group GLM linear (Eq. glm-linear): returns
+    (y_req [R, d_req] = act(W_RR x^R + b^R), y_cand [N, d_cand] = act(W_CR x^R_m + W_CC x^C + b^C))."""
+    lib = _lib.load()
+    _need(x_req is not None and x_req.dim() == 2, "x_req must be [R, k_req]")
+    n_req, k_req = x_req.shape
+    _need(w_rr.dim() == 2 and w_rr.shape[1] == k_req, "w_rr must be [d_req, k_req]")
+    d_req = w_rr.shape[0]
+    _need(w_rr.dtype == x_req.dtype and w_rr.is_contiguous(), "w_rr must match x_req")
+    if b_req is not None:
+        _need(b_req.dtype == torch.float32 and b_req.shape == (d_req,), "b_req must be float32 [d_req]")
+    if y_req is None:
+        y_req = torch.empty((n_req, d_req), dtype=x_req.dtype, device=x_req.device)
+    _need(y_req.shape == (n_req, d_req) and y_req.dtype == x_req.dtype and y_req.is_contiguous(),
+          "y_req must be a contiguous [R, d_req] tensor")
+    _on_gpu(x_req, w_rr, b_req, y_req)
+    y_cand = _linear(x_cand, w_cc, x_req, w_cr, cand_offsets, None, None, b_cand, activation,
+                     x_cand_add, y_cand, workspace, stream,
+                     request_side=(w_rr, b_req, y_req, d_req, lib))
+    return y_req, y_cand
+
+
 def _linear(x_cand, w_cand, x_req, w_req, cand_offsets, cand_ids, mapped, bias, activation,
-            x_cand_add, out, workspace, stream):
+            x_cand_add, out, workspace, stream, request_side=None):
     lib = _lib.load()
     _need(x_cand.dim() == 2 and w_cand.dim() == 2, "x_cand and w_cand must be 2-D")
     n_cand, k_cand = x_cand.shape
@@ -136,6 +160,14 @@ def _linear(x_cand, w_cand, x_req, w_req, cand_offsets, cand_ids, mapped, bias, 
     _on_gpu(x_cand, w_cand, x_req, w_req, index, bias, x_cand_add, out, workspace)
     _need(activation in _ACT, f"activation must be one of {sorted(k for k in _ACT if k)}")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if request_side is not None:
+        w_rr, b_req, y_req, d_req, _ = request_side
+        _lib.check(lib.rocs_glm_linear(
+            _ptr(x_req), k_req, _ptr(x_cand), _ptr(x_cand_add), k_cand, _ptr(w_rr), _ptr(w_req),
+            _ptr(w_cand), _ptr(b_req), _ptr(bias), _ptr(cand_offsets), n_req, n_cand, d_req,
+            d_out, code, _ACT[activation], _ptr(y_req), _ptr(out), _ptr(workspace), ws_bytes,
+            _stream(stream)), "rocs_glm_linear")
+        return out
     fn, name = ((lib.rocs_ikbo_linear_mapped, "rocs_ikbo_linear_mapped") if mapped
                 else (lib.rocs_ikbo_linear, "rocs_ikbo_linear"))
     _lib.check(fn(

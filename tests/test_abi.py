@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 14
+    assert len(names) == 15
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -53,6 +53,12 @@ def test_workspace_size(lib):
 P = ctypes.c_void_p
 FAKE = [P(0x10000 * (i + 1)) for i in range(12)]     # never dereferenced
 
+# The argument-error tests pass fake addresses that every call must reject
+# before it enqueues anything. They run where no GPU is visible, so a test
+# mistake can never turn into a kernel launch on those addresses.
+no_gpu = pytest.mark.skipif(__import__("torch").cuda.device_count() > 0,
+                            reason="fake-pointer argument checks run on hosts without a GPU")
+
 
 def _linear(lib, **kw):
     args = dict(x_req=FAKE[0], k_req=8, x_cand=FAKE[1], x_add=None, k_cand=8, w_req=FAKE[2],
@@ -62,6 +68,7 @@ def _linear(lib, **kw):
     return lib.rocs_ikbo_linear(*args.values())
 
 
+@no_gpu
 def test_linear_argument_errors(lib):
     assert _linear(lib, dtype=7) == _lib.INVALID_ARGUMENT
     assert b"dtype" in lib.rocs_last_error_message()
@@ -81,6 +88,7 @@ def test_linear_argument_errors(lib):
     assert lib.rocs_last_error_message() == b""
 
 
+@no_gpu
 def test_attention_argument_errors(lib):
     def call(**kw):
         a = dict(q=FAKE[0], k=FAKE[1], v=FAKE[2], co=FAKE[3], ko=FAKE[4], R=2, N=4, T=1, H=2,
@@ -97,6 +105,7 @@ def test_attention_argument_errors(lib):
     assert call(N=0) == _lib.OK
 
 
+@no_gpu
 def test_mapped_entry_points_argument_errors(lib):
     def lin(**kw):
         a = dict(x_req=FAKE[0], k_req=8, x_cand=FAKE[1], x_add=None, k_cand=8, w_req=FAKE[2],
@@ -121,6 +130,26 @@ def test_mapped_entry_points_argument_errors(lib):
     assert att(N=0) == _lib.OK
 
 
+@no_gpu
+def test_glm_linear_argument_errors(lib):
+    def call(**kw):
+        a = dict(x_req=FAKE[0], k_req=8, x_cand=FAKE[1], x_add=None, k_cand=8, w_rr=FAKE[2],
+                 w_cr=FAKE[3], w_cc=FAKE[4], b_r=None, b_c=None, off=FAKE[5], R=2, N=16,
+                 d_req=8, d_cand=8, dtype=1, act=1, y_req=FAKE[6], y_cand=FAKE[7], ws=FAKE[8],
+                 ws_bytes=1 << 20, stream=None)
+        a.update(kw)
+        return lib.rocs_glm_linear(*a.values())
+    assert call(y_req=None) == _lib.INVALID_ARGUMENT
+    assert call(w_rr=None) == _lib.INVALID_ARGUMENT
+    assert call(k_req=0, x_req=None) == _lib.INVALID_ARGUMENT
+    assert call(d_req=0) == _lib.INVALID_ARGUMENT
+    assert call(ws_bytes=16) == _lib.WORKSPACE_TOO_SMALL
+    assert call(y_req=FAKE[0]) == _lib.INVALID_ARGUMENT          # y_req aliases x_req
+    assert call(y_req=P(0x80000 + 8)) == _lib.INVALID_ARGUMENT   # y_req overlaps y_cand
+    assert call(R=0, N=0) == _lib.OK
+
+
+@no_gpu
 def test_lcb_argument_errors(lib):
     def call(fn=lib.rocs_ikbo_lcb, **kw):
         a = dict(xr=FAKE[0], xc=FAKE[1], wrr=FAKE[2], wcr=FAKE[3], wcc=FAKE[4], co=FAKE[5], R=2,
@@ -144,6 +173,7 @@ def test_lcb_argument_errors(lib):
     assert call(R=0, N=0) == _lib.OK
 
 
+@no_gpu
 def test_interaction_argument_errors(lib):
     def call(**kw):
         a = dict(xr=FAKE[0], xc=FAKE[1], co=FAKE[2], R=2, N=4, fr=16, fc=8, e=32, dtype=1,
@@ -158,6 +188,7 @@ def test_interaction_argument_errors(lib):
     assert call(R=0, N=0) == _lib.OK
 
 
+@no_gpu
 def test_request_ids_and_validate_errors(lib):
     assert lib.rocs_request_ids(FAKE[0], 0, 5, FAKE[1], None) == _lib.INVALID_ARGUMENT
     assert lib.rocs_request_ids(None, 2, 5, FAKE[1], None) == _lib.INVALID_ARGUMENT

@@ -159,3 +159,38 @@ def test_mapped_index_probe_and_clamp(gpu_lib):
                                      x_req=dtype(x_req), w_req=dtype(w_req),
                                      cand_request_ids=dev_i32(m))
         np.testing.assert_array_equal(host(out)[:, 0], np.clip(m, 0, r - 1) + (m < 0) * (r - 1))
+
+
+@pytest.mark.parametrize("shape", [([300, 0, 1, 211, 17], 96, 64, 160, 48),
+                                   ([20000, 13000, 17001], 256, 128, 516, 1024),
+                                   ([9, 0, 40], 13, 5, 7, 6)],
+                         ids=["small", "large", "general"])
+def test_glm_linear_full_layer(gpu_lib, shape):
+    # Both output groups of Eq. glm-linear; the request side comes from the
+    # stacked [W_RR; W_CR] request GEMM (the general path where K is odd).
+    counts, kr, kc, d, d_req = shape
+    case = wl.linear_case(counts, kr, kc, d, seed=61 + d, bias_std=0.3)
+    rng = np.random.default_rng(d_req)
+    w_rr = round_bf16(rng.standard_normal((d_req, kr)) / np.sqrt(kr)).astype(np.float32)
+    b_r = rng.standard_normal(d_req).astype(np.float32) * 0.3
+    y_req, y_cand = ops.glm_linear(dev_bf16(case.x_req), dev_bf16(case.x_cand), dev_bf16(w_rr),
+                                   dev_bf16(case.w_req), dev_bf16(case.w_cand),
+                                   dev_i32(case.cand_offsets), b_req=dev_f32(b_r),
+                                   b_cand=dev_f32(case.bias), activation="relu")
+    want_r, want_c = ikbo.glm_linear(case.x_req, case.x_cand, w_rr, case.w_req, case.w_cand,
+                                     b_r, case.bias, case.cand_offsets, "relu")
+    assert_close(host(y_cand), round_bf16(want_c), f"glm y_cand {shape}")
+    assert_close(host(y_req), round_bf16(want_r), f"glm y_req {shape}")
+
+
+def test_glm_linear_request_only(gpu_lib):
+    # No candidates: the request-side output is still produced.
+    case = wl.linear_case([0, 0, 0], 64, 32, 128, seed=70)
+    w_rr = round_bf16(np.random.default_rng(1).standard_normal((40, 64)) / 8).astype(np.float32)
+    y_req, y_cand = ops.glm_linear(dev_bf16(case.x_req), dev_bf16(case.x_cand), dev_bf16(w_rr),
+                                   dev_bf16(case.w_req), dev_bf16(case.w_cand),
+                                   dev_i32(case.cand_offsets))
+    want_r, _ = ikbo.glm_linear(case.x_req, case.x_cand, w_rr, case.w_req, case.w_cand, None,
+                                None, case.cand_offsets)
+    assert y_cand.shape == (0, 128)
+    assert_close(host(y_req), round_bf16(want_r), "glm request only")

@@ -181,6 +181,28 @@ def test_request_map_is_permutation_equivariant_and_checked():
             ikbo.ikbo_linear(x_req, x_cand, w_req, w_cand, None, None, request_map=bad)
 
 
+def test_glm_linear_full_layer():
+    # Brute force of both output groups (Eq. glm-linear, K = 2), and the
+    # GLM invariant: y^R never depends on any candidate.
+    rng = np.random.default_rng(25)
+    off = np.array([0, 3, 3, 5])
+    x_req, x_cand = rng.standard_normal((3, 4)), rng.standard_normal((5, 3))
+    w_rr, w_cr, w_cc = (rng.standard_normal((2, 4)), rng.standard_normal((6, 4)),
+                        rng.standard_normal((6, 3)))
+    b_r, b_c = rng.standard_normal(2), rng.standard_normal(6)
+    for act in ("none", "relu"):
+        y_req, y_cand = ikbo.glm_linear(x_req, x_cand, w_rr, w_cr, w_cc, b_r, b_c, off, act)
+        for r in range(3):
+            for d in range(2):
+                acc = b_r[d] + sum(w_rr[d, k] * x_req[r, k] for k in range(4))
+                assert abs(y_req[r, d] - (max(acc, 0.0) if act == "relu" else acc)) < 1e-12
+        np.testing.assert_allclose(
+            y_cand, _brute_linear(x_req, x_cand, w_cr, w_cc, b_c, off, act), rtol=1e-13,
+            atol=1e-13)
+        y2, _ = ikbo.glm_linear(x_req, -3.0 * x_cand, w_rr, w_cr, w_cc, b_r, b_c, off, act)
+        np.testing.assert_array_equal(y2, y_req)
+
+
 def test_plain_linear_is_matmul():
     rng = np.random.default_rng(4)
     x, w, b = rng.standard_normal((8, 6)), rng.standard_normal((5, 6)), rng.standard_normal(5)
