@@ -100,6 +100,14 @@ const char* rocs_last_error_message(void);
  * Fast path: bf16, k_req and k_cand multiples of 8, d_out a multiple of 4 and
  * every pointer 16-byte aligned. Other shapes take a slower general kernel
  * (the zero-padding transform of Section 4.2.4 restores the fast path).
+ *
+ * Environment: ROCS_LINEAR_COMBINED=1 runs the request-side GEMM inside the
+ * candidate kernel (one launch, Section 4.2.3) when the streaming candidate
+ * kernel applies (k_cand a multiple of 64, no x_cand_add): request tiles
+ * first, per-tile completion flags with agent-scope release / acquire. The
+ * workspace then also holds the flags (rocs_ikbo_linear_workspace_size
+ * covers them). Off by default: on MI355X the cross-XCD L2 write-back and
+ * invalidate cost more than the launch saved.
  * ---------------------------------------------------------------------------
  */
 size_t rocs_ikbo_linear_workspace_size(int64_t num_requests, int64_t num_cand,

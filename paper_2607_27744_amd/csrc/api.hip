@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
+#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -68,8 +69,13 @@ const char* rocs_last_error_message(void) { return g_error.c_str(); }
 size_t rocs_ikbo_linear_workspace_size(int64_t num_requests, int64_t num_cand, int64_t d_out,
                                        int64_t k_req) {
   if (k_req <= 0 || num_requests <= 0 || num_cand <= 0 || d_out <= 0) return 0;
+  // Request table Z [R, d_out] fp32, then one region that holds either the
+  // expanded index map [N] int32 or the combined kernel's completion flags
+  // (one 64-bit word per 16 x 16 tile of Z).
+  const size_t ids = (size_t)num_cand * sizeof(int32_t);
+  const size_t flags = (size_t)((num_requests + 15) / 16) * (size_t)((d_out + 15) / 16) * 8;
   return align256((size_t)num_requests * (size_t)d_out * sizeof(float)) +
-         align256((size_t)num_cand * sizeof(int32_t));
+         align256(ids > flags ? ids : flags);
 }
 
 }  // extern "C"
@@ -178,6 +184,8 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
   a.relu = activation == ROCS_ACT_RELU;
   a.out = out;
   a.w_rr = rs.w_rr; a.b_rr = rs.b_rr; a.y_req = rs.y_req; a.d_req = rs.d_req;
+  const char* combined = getenv("ROCS_LINEAR_COMBINED");
+  a.combined = combined != nullptr && combined[0] == '1';
   if (need > 0) {
     a.z = static_cast<float*>(workspace);
     a.ids = mapped ? const_cast<int32_t*>(cand_ids)

@@ -25,6 +25,7 @@ struct LinearArgs {
   const float* b_rr; // [d_req] or NULL
   void* y_req;       // [R, d_req] or NULL (candidate output only)
   int64_t d_req;
+  bool combined;     // run the request side inside the streaming candidate kernel
 };
 
 struct AttentionArgs {

@@ -16,6 +16,9 @@
 #include "kernels.h"
 #include "launch.h"
 
+#include <atomic>
+#include <random>
+
 namespace rocs {
 namespace {
 
@@ -46,25 +49,22 @@ struct RequestOut {          // the optional Y^R part of the stacked weight
   int d, tiles, relu;        // tiles = ceil(d / 16); 0 when there is no Y^R
 };
 
-__global__ __launch_bounds__(256) void request_gemm_bf16(
-    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w_in, const float* __restrict__ bias_in,
-    float* __restrict__ z, const int32_t* __restrict__ off, int32_t* __restrict__ ids, int R,
-    int64_t N, int K, int D_in, int tiles_d, int z_blocks, RequestOut yr) {
+// One 16 x 16 output tile `tile` of the stacked request GEMM, by a 256-thread
+// workgroup; `red` is 4 KiB of LDS. Returns whether the tile was a Zb tile
+// (the candidate side's input) and, for wave 0, its (row block, column block).
+__device__ __forceinline__ bool request_tile(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w_in,
+    const float* __restrict__ bias_in, float* __restrict__ z, int R, int K, int D_in,
+    int tiles_d, const RequestOut& yr, int tile, ROCS_LDS f32x4* red) {
   const int tid = threadIdx.x;
-  if ((int)blockIdx.x >= z_blocks) {
-    const int64_t n = (int64_t)(blockIdx.x - z_blocks) * 256 + tid;
-    if (n < N) ids[n] = owner_of(off, R, n);
-    return;
-  }
-  __shared__ f32x4 red[4][kWave];
   const int lane = tid & 63, wave = tid >> 6;
   const int tiles_all = yr.tiles + tiles_d;
-  const int t = (int)blockIdx.x % tiles_all;
+  const int t = tile % tiles_all;
   const bool to_y = t < yr.tiles;                 // a column tile of Y^R
   const bf16_t* w = to_y ? yr.w : w_in;
   const float* bias = to_y ? yr.bias : bias_in;
   const int D = to_y ? yr.d : D_in;
-  const int r0 = ((int)blockIdx.x / tiles_all) * 16, d0 = (to_y ? t : t - yr.tiles) * 16;
+  const int r0 = (tile / tiles_all) * 16, d0 = (to_y ? t : t - yr.tiles) * 16;
   const int row = lane & 15, kq = (lane >> 4) * 8;
   const bool dok = d0 + row < D, rok = r0 + row < R;
   const bf16_t* wp = w + (int64_t)(d0 + row) * K + kq;
@@ -77,10 +77,10 @@ __global__ __launch_bounds__(256) void request_gemm_bf16(
     const bf16x8 b = as_bf16x8(load16(xp + k, rok && kok));
     acc = mfma16(a, b, acc);   // acc[i] = Z[r0 + row][d0 + 4 (lane / 16) + i]
   }
-  red[wave][lane] = acc;
+  red[wave * kWave + lane] = acc;
   __syncthreads();
   if (wave == 0) {
-    f32x4 s = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+    f32x4 s = ((red[lane] + red[kWave + lane]) + red[2 * kWave + lane]) + red[3 * kWave + lane];
     const int d = d0 + (lane >> 4) * 4;
     if (rok && d < D) {
       if (bias != nullptr) s += *reinterpret_cast<const f32x4*>(bias + d);
@@ -93,6 +93,20 @@ __global__ __launch_bounds__(256) void request_gemm_bf16(
       }
     }
   }
+  return !to_y;
+}
+
+__global__ __launch_bounds__(256) void request_gemm_bf16(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ w_in, const float* __restrict__ bias_in,
+    float* __restrict__ z, const int32_t* __restrict__ off, int32_t* __restrict__ ids, int R,
+    int64_t N, int K, int D_in, int tiles_d, int z_blocks, RequestOut yr) {
+  if ((int)blockIdx.x >= z_blocks) {
+    const int64_t n = (int64_t)(blockIdx.x - z_blocks) * 256 + threadIdx.x;
+    if (n < N) ids[n] = owner_of(off, R, n);
+    return;
+  }
+  __shared__ f32x4 red[4 * kWave];
+  request_tile(x, w_in, bias_in, z, R, K, D_in, tiles_d, yr, (int)blockIdx.x, (ROCS_LDS f32x4*)red);
 }
 
 // ---------------------------------------------------------------------------
@@ -347,12 +361,47 @@ __device__ __forceinline__ bool stream_seek(StreamTile& c, StreamStep st, int n_
   return false;
 }
 
-template <bool HAS_ZB, bool RELU>
+// The request side inside the candidate kernel (Section 4.2.3, combined
+// request and candidate kernels): the stacked request GEMM's 16 x 16 tiles
+// are computed first, by the workgroups taken in ascending order, and each
+// Zb tile publishes a completion flag (agent-scope release: the tile's
+// stores reach every XCD before the flag does). A workgroup then issues its
+// first candidate loads and waits for the flags while they are in flight,
+// then fences once (agent-scope acquire); the main loop and the epilogue
+// carry no request-side state. Flags hold this call's epoch (a per-process
+// random salt and a call counter), so stale flags from earlier calls never
+// match and nothing resets them. The wait is bounded: past the limit the
+// workgroup computes every tile whose flag is still unset itself (the same
+// code, so the same values), so every workgroup always finishes.
+struct FusedRequest {
+  const bf16_t* x;           // x_req [R, K]
+  const bf16_t* w;           // W_CR [D, K]
+  const float* bias;         // b [D] or NULL
+  float* z;                  // Zb [R, D] (workspace)
+  RequestOut yr;             // optional Y^R part of the stacked weight
+  uint64_t* flags;           // one per Zb tile: ceil(R / 16) x ceil(D / 16)
+  uint64_t epoch;
+  int K, tiles_d, n_tiles;   // n_tiles: all request tiles (Y^R and Zb)
+};
+
+constexpr int kFlagSpinLimit = 1 << 17;   // polls of about 0.3 us each
+
+// This call's flag value: a per-process random salt in the high word and a
+// call counter below it (never zero).
+uint64_t next_epoch() {
+  static std::atomic<uint64_t> counter{[] {
+    std::random_device rd;
+    return (uint64_t)rd() << 32 | 1u;
+  }()};
+  return counter.fetch_add(1, std::memory_order_relaxed);
+}
+
+template <bool HAS_ZB, bool RELU, bool FUSED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
                       const float* __restrict__ zb, const int32_t* __restrict__ off_g,
                       bf16_t* __restrict__ out, int R, int64_t N, int K, int D, int tiles_m,
-                      int n_slots, StreamStep step_g) {
+                      int n_slots, StreamStep step_g, FusedRequest fr) {
   constexpr int BM = kStreamBM, BN = kStreamBN, BK = kStreamBK;
   constexpr int NSA = 2, NSB = 3;                // ring depths: weights, candidates
   constexpr int ROWB = BK * 2;                   // bytes of one slab row (128)
@@ -375,7 +424,26 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   const int wm0 = (wave & 1) * 128, wn0 = (wave >> 1) * 128;
   const int nk = K / BK;
   const int rowb = K * 2;
-  const int first = (int)xcd_remap(blockIdx.x, gridDim.x);
+  const int logical = (int)xcd_remap(blockIdx.x, gridDim.x);
+  // Request tiles reduce through the third candidate ring slot, which the
+  // prologue leaves empty.
+  ROCS_LDS f32x4* const red = (ROCS_LDS f32x4*)(lds3 + BBASE + 2 * SLAB);
+  auto run_request_tile = [&](int t) __attribute__((always_inline)) {
+    const bool is_zb = request_tile(fr.x, fr.w, fr.bias, fr.z, R, fr.K, D, fr.tiles_d, fr.yr,
+                                    t, red);
+    if (is_zb && threadIdx.x == 0) {      // wave 0 stored the tile
+      const int tiles_all = fr.yr.tiles + fr.tiles_d;
+      const int fi = (t / tiles_all) * fr.tiles_d + (t % tiles_all - fr.yr.tiles);
+      __hip_atomic_store(fr.flags + fi, fr.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+  };
+  if constexpr (FUSED) {
+    for (int t = logical; t < fr.n_tiles; t += (int)gridDim.x) run_request_tile(t);
+  }
+  // Candidate tiles: descending for the workgroups that took request tiles
+  // (they get the smaller share when the tiles do not divide evenly).
+  const int first = FUSED ? (int)gridDim.x - 1 - logical : logical;
   const uint32_t lbase = lds_addr(lds);
 
   // DMA lane map: load i of this wave fills slab rows RPI (NI wave + i) +
@@ -504,6 +572,41 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     }
   };
 
+  // Combined kernel: wait (bounded) until every Zb tile's flag carries this
+  // call's epoch; past the limit, compute the missing tiles here.
+  auto wait_request_side = [&]() __attribute__((always_inline)) {
+    const int nflags = ((R + 15) / 16) * fr.tiles_d;
+    int spins = 0;
+    for (; spins < kFlagSpinLimit; ++spins) {
+      bool ok = true;
+      for (int i = lane; i < nflags; i += kWave)
+        ok &= __hip_atomic_load(fr.flags + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == fr.epoch;
+      if (__ballot(!ok) == 0) break;
+      __builtin_amdgcn_s_sleep(8);
+    }
+    // Workgroup-wide verdicts go through one LDS word past the reduction
+    // area, so every wave takes the same branch around the tiles' barriers.
+    ROCS_LDS int* const verdict = (ROCS_LDS int*)(lds3 + BBASE + 2 * SLAB + 4096);
+    if (threadIdx.x == 0) *verdict = 0;
+    __syncthreads();
+    if (lane == 0 && spins == kFlagSpinLimit) *verdict = 1;
+    __syncthreads();
+    const bool timed_out = *verdict != 0;
+    __syncthreads();
+    if (timed_out) {
+      const int tiles_all = fr.yr.tiles + fr.tiles_d;
+      for (int fi = 0; fi < nflags; ++fi) {
+        if (threadIdx.x == 0)
+          *verdict = __hip_atomic_load(fr.flags + fi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != fr.epoch;
+        __syncthreads();
+        const bool run = *verdict != 0;
+        __syncthreads();
+        if (run) run_request_tile((fi / fr.tiles_d) * tiles_all + fr.yr.tiles + fi % fr.tiles_d);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  };
+
   // Epilogue. Element 4 q + i of acc[fm][fn] is feature 32 fm + 8 q + h4 + i
   // of candidate 32 fn + l32 (within the wave's quarter). For q = 2j, 2j + 1
   // the lower half-wave keeps its q = 2j words and takes the upper half's,
@@ -591,6 +694,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     for (int i = 0; i < NI; ++i) dma_piece(pb_src, pb_lim, pb_dst, i);
   }
   pa_on = pb_on = false;
+  if constexpr (FUSED) wait_request_side();   // while the first slabs load
   wait_vmcnt<0>();
   ring_barrier();
 
@@ -748,19 +852,24 @@ hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
                       a.k_cand < (int64_t(1) << 22) &&
                       ((a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN) *
                               ((a.d_out + kStreamBM - 1) / kStreamBM) < (int64_t(1) << 31);
-  if (a.k_req > 0) {
-    RequestOut yr{static_cast<const bf16_t*>(a.w_rr), a.b_rr, static_cast<bf16_t*>(a.y_req),
-                  (int)a.d_req, a.y_req != nullptr ? (int)((a.d_req + 15) / 16) : 0,
-                  (int)a.relu};
-    // No candidates: only the Y^R tiles (the request table has no reader).
-    const int tiles_d = a.N > 0 ? (int)((a.d_out + 15) / 16) : 0;
-    const int z_blocks = (yr.tiles + tiles_d) * (int)((a.R + 15) / 16);
+  // On request, the streaming kernel also runs the request side (combined
+  // kernel); otherwise the request GEMM is a launch of its own. Separate
+  // launches are the default on this part: the cross-XCD release / acquire
+  // the combined kernel needs (an L2 write-back per request tile, an L2
+  // invalidate per workgroup) costs more than the launch it saves.
+  const bool fused = a.combined && stream && a.k_req > 0 && a.N > 0;
+  RequestOut yr{static_cast<const bf16_t*>(a.w_rr), a.b_rr, static_cast<bf16_t*>(a.y_req),
+                (int)a.d_req, a.y_req != nullptr ? (int)((a.d_req + 15) / 16) : 0, (int)a.relu};
+  // No candidates: only the Y^R tiles (the request table has no reader).
+  const int tiles_d = a.N > 0 ? (int)((a.d_out + 15) / 16) : 0;
+  const int req_tiles = (yr.tiles + tiles_d) * (int)((a.R + 15) / 16);
+  if (a.k_req > 0 && !fused) {
     const int id_blocks = stream || a.ids_given ? 0 : (int)((a.N + 255) / 256);
-    hipError_t e = launch_kernel(request_gemm_bf16, dim3(z_blocks + id_blocks), dim3(256), s,
+    hipError_t e = launch_kernel(request_gemm_bf16, dim3(req_tiles + id_blocks), dim3(256), s,
                                  static_cast<const bf16_t*>(a.x_req),
                                  static_cast<const bf16_t*>(a.w_req), a.bias, a.z,
                                  a.cand_offsets, a.ids, (int)a.R, a.N, (int)a.k_req,
-                                 (int)a.d_out, tiles_d, z_blocks, yr);
+                                 (int)a.d_out, tiles_d, req_tiles, yr);
     if (e != hipSuccess) return e;
   }
   if (a.N == 0) return hipSuccess;      // request-side output only
@@ -779,12 +888,29 @@ hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
     const bf16_t* x = static_cast<const bf16_t*>(a.x_cand);
     const bf16_t* w = static_cast<const bf16_t*>(a.w_cand);
     bf16_t* o = static_cast<bf16_t*>(a.out);
+    FusedRequest fr{};
+    if (fused) {
+      fr.x = static_cast<const bf16_t*>(a.x_req);
+      fr.w = static_cast<const bf16_t*>(a.w_req);
+      fr.bias = a.bias;
+      fr.z = a.z;
+      fr.yr = yr;
+      fr.flags = reinterpret_cast<uint64_t*>(a.ids);   // the index map's slot is free here
+      fr.epoch = next_epoch();
+      fr.K = (int)a.k_req;
+      fr.tiles_d = tiles_d;
+      fr.n_tiles = req_tiles;
+    }
     auto go = [&](auto kernel) {
       return launch_kernel(kernel, dim3((uint32_t)grid), dim3(256), s, x, w, zb, off, o,
-                           (int)a.R, a.N, (int)a.k_cand, (int)a.d_out, tiles_m, (int)slots, step);
+                           (int)a.R, a.N, (int)a.k_cand, (int)a.d_out, tiles_m, (int)slots, step,
+                           fr);
     };
-    if (zb != nullptr) return a.relu ? go(ikbo_gemm_stream<true, true>) : go(ikbo_gemm_stream<true, false>);
-    return a.relu ? go(ikbo_gemm_stream<false, true>) : go(ikbo_gemm_stream<false, false>);
+    if (fused)
+      return a.relu ? go(ikbo_gemm_stream<true, true, true>) : go(ikbo_gemm_stream<true, false, true>);
+    if (zb != nullptr)
+      return a.relu ? go(ikbo_gemm_stream<true, true, false>) : go(ikbo_gemm_stream<true, false, false>);
+    return a.relu ? go(ikbo_gemm_stream<false, true, false>) : go(ikbo_gemm_stream<false, false, false>);
   }
   // Large tiles when they still give every CU at least four tiles. The bias
   // is already inside Z when there is a request term.

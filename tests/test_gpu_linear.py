@@ -194,3 +194,32 @@ def test_glm_linear_request_only(gpu_lib):
                                 None, case.cand_offsets)
     assert y_cand.shape == (0, 128)
     assert_close(host(y_req), round_bf16(want_r), "glm request only")
+
+
+@pytest.mark.parametrize("shape", [([300, 0, 1, 211, 17], 96, 64, 256),
+                                   ([2000, 13000, 0, 17001], 256, 128, 516)],
+                         ids=["small", "large"])
+def test_combined_request_candidate_kernel(gpu_lib, shape, monkeypatch):
+    # ROCS_LINEAR_COMBINED=1: request tiles inside the streaming kernel with
+    # completion flags (and Y^R from the stacked weight); equal to the
+    # separate launches and to the oracle, on two calls with one workspace
+    # (the second call's flags must not match the first call's epoch).
+    counts, kr, kc, d = shape
+    case = wl.linear_case(counts, kr, kc, d, seed=91 + d, bias_std=0.3)
+    n = case.x_cand.shape[0]
+    ws = torch.zeros(ops.linear_workspace_size(len(counts), n, d, kr), dtype=torch.uint8,
+                     device="cuda")
+    w_rr = round_bf16(np.random.default_rng(3).standard_normal((32, kr)) / np.sqrt(kr)).astype(np.float32)
+    args = (dev_bf16(case.x_req), dev_bf16(case.x_cand), dev_bf16(w_rr), dev_bf16(case.w_req),
+            dev_bf16(case.w_cand), dev_i32(case.cand_offsets))
+    kw = dict(b_cand=dev_f32(case.bias), activation="relu")
+    sep_r, sep_c = ops.glm_linear(*args, **kw)
+    monkeypatch.setenv("ROCS_LINEAR_COMBINED", "1")
+    want_r, want_c = ikbo.glm_linear(case.x_req, case.x_cand, w_rr, case.w_req, case.w_cand,
+                                     None, case.bias, case.cand_offsets, "relu")
+    for _ in range(2):
+        y_r, y_c = ops.glm_linear(*args, workspace=ws, **kw)
+        assert_close(host(y_c), round_bf16(want_c), f"combined y_cand {shape}")
+        assert_close(host(y_r), round_bf16(want_r), f"combined y_req {shape}")
+        np.testing.assert_array_equal(host(y_c), host(sep_c))
+        np.testing.assert_array_equal(host(y_r), host(sep_r))
