@@ -1,6 +1,7 @@
 """Throughput benchmark of the IKBO hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 5] [--no-cpu-baseline]
+    python bench.py --variant NAME     (one operator variant; see variants.py)
 
 A step is one pass of the workload's whole hot path over one batch (default:
 workload 5, production-scale retrieval: 16 requests x 65,536 candidates; IKBO
@@ -212,12 +213,22 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--variant", default=None,
+                    help="time one operator variant instead of a workload step "
+                         "(lcb, dca_tq32, dca_tq64, dca_request, linear_mapped, "
+                         "linear_combined, glm_linear); prints its own JSON line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build has no multi-GPU path "
               f"(--gpus {args.gpus} requested). Requests shard independently across GPUs; "
               "see the design notes.", file=sys.stderr)
         sys.exit(2)
+
+    if args.variant is not None:
+        from paper_2607_27744_amd import variants
+        log(f"variant {args.variant}")
+        print(json.dumps(variants.run(args.variant, args.steps, args.warmup)), flush=True)
+        return
 
     import numpy as np
     import torch

@@ -294,8 +294,9 @@ int32_t rocs_glm_interaction(const void* x_req, const void* x_cand,
  * overlap inputs, each other or the workspace.
  *
  * Fast path (bf16 MFMA candidate kernel): bf16, f_cand in {16, 32, 64}, and
- * (emb_dim, o_cand) in {(128, 32), (64, 32), (64, 64)}, x_cand 16-byte and
- * w_cc / y_cand 8-byte aligned. Other cases run a general kernel.
+ * (emb_dim, o_cand) in {(128, 32), (64, 32), (64, 64)}, x_cand and y_cand
+ * 16-byte, w_cc, x_req and y_req 8-byte aligned. Other cases run a general
+ * kernel.
  * ---------------------------------------------------------------------------
  */
 size_t rocs_ikbo_lcb_workspace_size(int64_t num_requests, int64_t o_cand, int64_t emb_dim);

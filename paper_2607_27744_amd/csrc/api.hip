@@ -428,7 +428,8 @@ int32_t lcb_impl(const char* name, bool mapped, const void* x_req, const void* x
   a.y_req = o_req > 0 ? y_req : nullptr; a.y_cand = y_cand;
   a.z = static_cast<float*>(workspace);
   const bool fast = a.bf16 && rocs::lcb_fast_shape(f_cand, o_cand, emb) && aligned(x_cand, 16) &&
-                    aligned(w_cc, 8) && aligned(y_cand, 8);
+                    aligned(w_cc, 8) && aligned(y_cand, 16) && aligned(x_req, 8) &&
+                    aligned(y_req, 8);
   const hipError_t e = rocs::launch_lcb(a, fast, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
   return ok();

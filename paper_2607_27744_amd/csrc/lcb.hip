@@ -32,7 +32,13 @@ constexpr int kLcbStages = 2;    // per-wave LDS ring depth (candidate inputs)
 //       inside each 16-field step as the transposing read produces);
 //   C starts at Z_{m_n}, kept in registers while the request stays the same.
 // Each lane ends with runs of 4 consecutive embedding columns of one output
-// field: 8-byte stores, 16-byte Z loads.
+// field (16-byte Z loads). The output goes back through LDS: a half-wave
+// swap gives each lane 16 contiguous bytes, written into the candidate's
+// consumed input stage (XOR-swizzled by output row, conflict-free) and read
+// back row-contiguous, so each store instruction writes 1 KiB of the
+// candidate's contiguous output. Written straight from the MFMA layout, a
+// store instruction would touch 32 rows with 16 bytes each, and the write
+// path, not the matrix cores, would set the pace.
 //
 // Each wave owns a contiguous run of candidates and streams their inputs
 // through a private 2-deep LDS ring with the DMA form of the global load
@@ -48,15 +54,17 @@ void lcb_cand_bf16(const bf16_t* __restrict__ xc, const bf16_t* __restrict__ wcc
                    int64_t N, int per_wave) {
   constexpr int ROWB = 2 * E;                 // bytes of one field row
   constexpr int CR = ROWB / 16;               // 16-byte chunks per row
-  constexpr int SB = NK * ROWB;               // bytes of one candidate's input
   constexpr int KPI = 1024 / ROWB;            // field rows per wave-wide DMA load
   constexpr int NI = NK / KPI;                // DMA loads per candidate
   constexpr int KS = NK / 16;                 // MFMA steps over fields
   constexpr int MB = E / 32;                  // 32-wide embedding blocks
   constexpr int O = 32 * NOB;                 // output fields
-  constexpr int NS = MB * NOB * 4;            // 8-byte stores per lane per candidate
+  constexpr int SO = O * ROWB;                // bytes of one candidate's output
+  constexpr int NSO = SO / 1024;              // 1 KiB stores per candidate
+  // A stage holds a candidate's input, then its output on the way out.
+  constexpr int SB = NK * ROWB > SO ? NK * ROWB : SO;
   static_assert(NK % 16 == 0 && NK % KPI == 0 && (E == 64 || E == 128), "shape");
-  static_assert(NI + 2 * NS < 64, "vmcnt field");
+  static_assert(SO % 1024 == 0 && NI + NSO < 64, "output staging / vmcnt field");
   __shared__ __attribute__((aligned(1024))) char lds[kLcbWaves * kLcbStages * SB];
   ROCS_LDS char* const lds3 = (ROCS_LDS char*)lds;
 
@@ -151,13 +159,11 @@ void lcb_cand_bf16(const bf16_t* __restrict__ xc, const bf16_t* __restrict__ wcc
     }
     // Candidate c resident. Vector-memory operations retire in issue order,
     // so the wait allows exactly those issued after c's DMA loads: the
-    // stores of c - 2 (c >= 2), the loads of c + 1 (when there is a c + 1)
-    // and the stores of c - 1 (c >= 1). A smaller count would only wait
-    // longer; a larger one would not make c resident.
-    if (c >= 2) {
-      if (c + 1 < count) wait_vmcnt<2 * NS + NI>(); else wait_vmcnt<2 * NS>();
-    } else if (c == 1) {
-      if (count > 2) wait_vmcnt<NS + NI>(); else wait_vmcnt<NS>();
+    // stores of c - 1 (c >= 1) and the loads of c + 1 (when there is a
+    // c + 1). A smaller count would only wait longer; a larger one would not
+    // make c resident.
+    if (c >= 1) {
+      if (c + 1 < count) wait_vmcnt<NSO + NI>(); else wait_vmcnt<NSO>();
     } else {
       if (count > 1) wait_vmcnt<NI>(); else wait_vmcnt<0>();
     }
@@ -177,23 +183,49 @@ void lcb_cand_bf16(const bf16_t* __restrict__ xc, const bf16_t* __restrict__ wcc
         for (int ob = 0; ob < NOB; ++ob)
           acc[mb][ob] = mfma32(a, wf[s][ob], s == 0 ? zacc[mb][ob] : acc[mb][ob]);
       }
-    // Every read of this stage has returned before the next DMA overwrites it.
+    // Every transposing read of this stage has returned: it now takes the
+    // output. Element 4 q + i of acc[mb][ob] is column 32 mb + 8 q + 4 hh + i
+    // of output row 32 ob + l32; after the half-wave swap lane (l32, hh)
+    // holds columns 32 mb + 16 j + 8 hh .. +7 (16-byte chunk 4 mb + 2 j + hh).
     __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
     asm volatile("" ::: "memory");
-    if (c + 2 < count) issue(c + 2);
-    // Element 4 q + i of acc[mb][ob]: column 32 mb + 8 q + 4 hh + i of
-    // output field 32 ob + l32.
-    bf16_t* yr = yc + n * (int64_t)(O * E);
+    auto out_swz = [](int row) { return CR == 16 ? (row & 15) : ((row >> 1) & 7); };
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int ob = 0; ob < NOB; ++ob)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int j = 0; j < 2; ++j) {
           const f32x16& v = acc[mb][ob];
-          *reinterpret_cast<u32x2*>(yr + (int64_t)(32 * ob + l32) * E + 32 * mb + 8 * q + 4 * hh) =
-              u32x2{pack_bf16x2(v[4 * q], v[4 * q + 1]), pack_bf16x2(v[4 * q + 2], v[4 * q + 3])};
+          const uint32_t e0 = pack_bf16x2(v[8 * j], v[8 * j + 1]);
+          const uint32_t e1 = pack_bf16x2(v[8 * j + 2], v[8 * j + 3]);
+          const uint32_t o0 = pack_bf16x2(v[8 * j + 4], v[8 * j + 5]);
+          const uint32_t o1 = pack_bf16x2(v[8 * j + 6], v[8 * j + 7]);
+          const auto s0 = __builtin_amdgcn_permlane32_swap(e0, o0, false, false);
+          const auto s1 = __builtin_amdgcn_permlane32_swap(e1, o1, false, false);
+          const int row = 32 * ob + l32;
+          const int chunk = (4 * mb + 2 * j + hh) ^ out_swz(row);
+          *reinterpret_cast<ROCS_LDS u32x4*>(lds3 + sbase + row * ROWB + 16 * chunk) =
+              u32x4{s0[0], s1[0], s0[1], s1[1]};
         }
+    // Read back row-contiguous: store i covers rows (1024 / ROWB) i .. , lane
+    // -> row + lane / CR, chunk lane % CR; 1 KiB of contiguous output each.
+    u32x4 ov[NSO];
+#pragma unroll
+    for (int i = 0; i < NSO; ++i) {
+      const int row = (1024 / ROWB) * i + lane / CR;
+      ov[i] = *reinterpret_cast<const ROCS_LDS u32x4*>(
+          lds3 + sbase + row * ROWB + 16 * ((lane % CR) ^ out_swz(row)));
+    }
+    bf16_t* yr = yc + n * (int64_t)(O * E);
+#pragma unroll
+    for (int i = 0; i < NSO; ++i)
+      *reinterpret_cast<u32x4*>(reinterpret_cast<char*>(yr) + 1024 * i + 16 * lane) = ov[i];
+    // The stage is free once those reads have returned (the stores above
+    // consumed them); the DMA of candidate c + 2 refills it.
+    __builtin_amdgcn_s_waitcnt((0 << 8) | (7 << 4) | 15 | (3 << 14));
+    asm volatile("" ::: "memory");
+    if (c + 2 < count) issue(c + 2);
   }
 }
 
@@ -266,13 +298,56 @@ hipError_t dispatch_nk(const LcbArgs& a, hipStream_t s) {
   }
 }
 
+// Request side, bf16 with E a multiple of 4: each thread makes 4 adjacent
+// embedding columns of one output row (8-byte input loads shared across the
+// 4 columns, the weight row read once per field).
+__global__ __launch_bounds__(256) void lcb_request_bf16x4(
+    const bf16_t* __restrict__ xr, const bf16_t* __restrict__ wrr, const bf16_t* __restrict__ wcr,
+    bf16_t* __restrict__ yr, float* __restrict__ z, int R, int FR, int OR, int OC, int E) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int E4 = E / 4;
+  const int64_t per_req = (int64_t)(OR + OC) * E4;
+  if (idx >= (int64_t)R * per_req) return;
+  const int r = (int)(idx / per_req);
+  const int o = (int)((idx % per_req) / E4), e = 4 * (int)(idx % E4);
+  const bool req_out = o < OR;
+  const bf16_t* w = req_out ? wrr + (int64_t)o * FR : wcr + (int64_t)(o - OR) * FR;
+  const bf16_t* x = xr + (int64_t)r * FR * E + e;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll 4
+  for (int f = 0; f < FR; ++f) {
+    const float wf = (float)w[f];
+    const u32x2 v = *reinterpret_cast<const u32x2*>(x + (int64_t)f * E);
+    a0 = fmaf(wf, bf16_lo(v[0]), a0);
+    a1 = fmaf(wf, bf16_hi(v[0]), a1);
+    a2 = fmaf(wf, bf16_lo(v[1]), a2);
+    a3 = fmaf(wf, bf16_hi(v[1]), a3);
+  }
+  if (req_out) {
+    *reinterpret_cast<u32x2*>(yr + ((int64_t)r * OR + o) * E + e) =
+        u32x2{pack_bf16x2(a0, a1), pack_bf16x2(a2, a3)};
+  } else {
+    *reinterpret_cast<f32x4*>(z + ((int64_t)r * OC + (o - OR)) * E + e) = f32x4{a0, a1, a2, a3};
+  }
+}
+
 template <typename T>
 hipError_t launch_typed(const LcbArgs& a, bool fast, hipStream_t s) {
-  const int64_t req_elems = a.R * (int64_t)(a.o_req + a.o_cand) * a.emb;
-  hipError_t e = launch_kernel(lcb_request<T>, dim3((uint32_t)((req_elems + 255) / 256)), dim3(256),
-                               s, static_cast<const T*>(a.x_req), static_cast<const T*>(a.w_rr),
-                               static_cast<const T*>(a.w_cr), static_cast<T*>(a.y_req), a.z,
-                               (int)a.R, a.f_req, a.o_req, a.o_cand, a.emb);
+  hipError_t e;
+  if (std::is_same_v<T, bf16_t> && fast) {
+    // fast implies E in {64, 128} and 16-byte aligned rows
+    const int64_t req_threads = a.R * (int64_t)(a.o_req + a.o_cand) * (a.emb / 4);
+    e = launch_kernel(lcb_request_bf16x4, dim3((uint32_t)((req_threads + 255) / 256)), dim3(256),
+                      s, static_cast<const bf16_t*>(a.x_req), static_cast<const bf16_t*>(a.w_rr),
+                      static_cast<const bf16_t*>(a.w_cr), static_cast<bf16_t*>(a.y_req), a.z,
+                      (int)a.R, a.f_req, a.o_req, a.o_cand, a.emb);
+  } else {
+    const int64_t req_elems = a.R * (int64_t)(a.o_req + a.o_cand) * a.emb;
+    e = launch_kernel(lcb_request<T>, dim3((uint32_t)((req_elems + 255) / 256)), dim3(256),
+                      s, static_cast<const T*>(a.x_req), static_cast<const T*>(a.w_rr),
+                      static_cast<const T*>(a.w_cr), static_cast<T*>(a.y_req), a.z,
+                      (int)a.R, a.f_req, a.o_req, a.o_cand, a.emb);
+  }
   if (e != hipSuccess || a.N == 0) return e;
   if constexpr (std::is_same_v<T, bf16_t>) {
     if (fast) {
