@@ -369,20 +369,43 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
     last_stage((ntiles - 1) % kStages, s_a);
   }
 
+  // Epilogue through LDS. Once every wave is past its last stage the K/V
+  // ring is idle; each wave writes its 32 normalised output rows there
+  // (16 contiguous bytes per lane after a half-wave swap, row-swizzled) and
+  // reads them back row-contiguous, so each store instruction covers whole
+  // 2D-byte row segments instead of 16 bytes of 32 different rows.
+  ring_barrier();
   if (!active) return;
-  // Element 4 qq + i of oacc[db] is O[row l32][dim 32 db + 8 qq + 4 hh + i].
+  // Element 4 qq + i of oacc[db] is O[row l32][dim 32 db + 8 qq + 4 hh + i];
+  // after the swap lane (l32, hh) holds dims 32 db + 16 j + 8 hh .. +7
+  // (16-byte chunk 4 db + 2 j + hh of the row).
   const float inv = 1.0f / sum_across_halves(l_part);
-  const int rr = wrow0 + l32;
-  if (rr >= rows) return;
+  const uint32_t obase = (uint32_t)(wave * 32 * ROWB);
+  auto out_swz = [](int row) { return CR == 16 ? (row & 15) : ((row >> 1) & 7); };
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
+    for (int j = 0; j < 2; ++j) {
       const f32x16& o = oacc[db];
-      *reinterpret_cast<u32x2*>(oh + rr * qs + 32 * db + 8 * qq + 4 * hh) =
-          u32x2{pack_bf16x2(o[4 * qq] * inv, o[4 * qq + 1] * inv),
-                pack_bf16x2(o[4 * qq + 2] * inv, o[4 * qq + 3] * inv)};
+      const uint32_t e0 = pack_bf16x2(o[8 * j] * inv, o[8 * j + 1] * inv);
+      const uint32_t e1 = pack_bf16x2(o[8 * j + 2] * inv, o[8 * j + 3] * inv);
+      const uint32_t o0 = pack_bf16x2(o[8 * j + 4] * inv, o[8 * j + 5] * inv);
+      const uint32_t o1 = pack_bf16x2(o[8 * j + 6] * inv, o[8 * j + 7] * inv);
+      const auto s0 = __builtin_amdgcn_permlane32_swap(e0, o0, false, false);
+      const auto s1 = __builtin_amdgcn_permlane32_swap(e1, o1, false, false);
+      const int chunk = (4 * db + 2 * j + hh) ^ out_swz(l32);
+      *reinterpret_cast<ROCS_LDS u32x4*>(lds3 + obase + l32 * ROWB + 16 * chunk) =
+          u32x4{s0[0], s1[0], s0[1], s1[1]};
     }
+  constexpr int RPS = 1024 / ROWB;            // output rows per store instruction
+#pragma unroll
+  for (int i = 0; i < 32 / RPS; ++i) {
+    const int row = RPS * i + lane / CR;
+    const u32x4 v = *reinterpret_cast<const ROCS_LDS u32x4*>(
+        lds3 + obase + row * ROWB + 16 * ((lane % CR) ^ out_swz(row)));
+    if (wrow0 + row < rows)
+      *reinterpret_cast<u32x4*>(oh + (int64_t)(wrow0 + row) * qs + 8 * (lane % CR)) = v;
+  }
 }
 
 // ---------------------------------------------------------------------------
