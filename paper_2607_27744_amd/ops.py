@@ -197,8 +197,19 @@ def dca_request_attention(q_req, k, v, kv_offsets, *, scale=None, out=None, stre
     _need(q_req.dim() == 4, "q_req must be [R, T, H, d]")
     n_req = q_req.shape[0]
     _need(kv_offsets.numel() == n_req + 1, "kv_offsets needs R + 1 entries")
-    ident = torch.arange(n_req + 1, dtype=torch.int32, device=q_req.device)
-    return _attention(q_req, k, v, ident, None, kv_offsets, scale, out, stream)
+    return _attention(q_req, k, v, _identity_offsets(n_req, q_req.device), None, kv_offsets,
+                      scale, out, stream)
+
+
+_IDENTITY = {}
+
+
+def _identity_offsets(n_req, device):
+    """[0, 1, ..., R] int32 on the device, built once per (R, device)."""
+    key = (n_req, str(device))
+    if key not in _IDENTITY:
+        _IDENTITY[key] = torch.arange(n_req + 1, dtype=torch.int32, device=device)
+    return _IDENTITY[key]
 
 
 def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream):
