@@ -117,3 +117,32 @@ def production_retrieval(w, rows=None):
 
 PIPELINES = {1: tiny_block, 2: retrieval_mlp, 3: ranking_dca, 4: fm_linear,
              5: production_retrieval}
+
+
+def dca_layer(w):
+    """One full DCA layer (Section 3.2), composed from the oracle operators.
+
+    ROCSified query generation (Eq. dca-query): [Z^R; Z^C] = LCB([Y^R; Y^C])
+    (Eq. glm-lcb-two-groups), flattened per row, then a two-layer GLM MLP
+    (Eq. glm-linear; ReLU after the first layer) gives [Q^R; Q^C] with
+    q_len x heads x head_dim per row. Group-wise cross attention
+    (Eq. dca-attention): A^R = Attn(Q^R, S W_K^R, S W_V^R) per request and
+    A^C = Attn(Q^C, S W_K^C, S W_V^C) per candidate over its request's
+    sequence. bf16 rounding at every operator boundary, as on the GPU.
+    """
+    r, n = w.y_req.shape[0], w.y_cand.shape[0]
+    t, h, d = w.q_len, w.heads, w.head_dim
+    z_r, z_c = ikbo.glm_lcb(w.y_req, w.y_cand, w.lcb_rr, w.lcb_cr, w.lcb_cc, w.cand_offsets)
+    z_r, z_c = round_bf16(z_r).reshape(r, -1), round_bf16(z_c).reshape(n, -1)
+    h_r, h_c = ikbo.glm_linear(z_r, z_c, w.w1_rr, w.w1_cr, w.w1_cc, w.b1_r, w.b1_c,
+                               w.cand_offsets, "relu")
+    h_r, h_c = round_bf16(h_r), round_bf16(h_c)
+    q_r, q_c = ikbo.glm_linear(h_r, h_c, w.w2_rr, w.w2_cr, w.w2_cc, None, None, w.cand_offsets)
+    q_r, q_c = round_bf16(q_r).reshape(r, t, h, d), round_bf16(q_c).reshape(n, t, h, d)
+    k_r = round_bf16(ikbo.sequence_projection(w.s, w.wk_r)).reshape(-1, h, d)
+    v_r = round_bf16(ikbo.sequence_projection(w.s, w.wv_r)).reshape(-1, h, d)
+    k_c = round_bf16(ikbo.sequence_projection(w.s, w.wk_c)).reshape(-1, h, d)
+    v_c = round_bf16(ikbo.sequence_projection(w.s, w.wv_c)).reshape(-1, h, d)
+    a_r = ikbo.dca_attention(q_r, k_r, v_r, np.arange(r + 1), w.kv_offsets)
+    a_c = ikbo.dca_attention(q_c, k_c, v_c, w.cand_offsets, w.kv_offsets, mode="grouped")
+    return {"q_req": q_r, "q_cand": q_c, "a_req": round_bf16(a_r), "a_cand": round_bf16(a_c)}

@@ -152,3 +152,43 @@ def outputs(p):
         4: lambda: {"y_req": p.y_req, "y_cand": p.y_cand, "out": p.out},
         5: lambda: {"h1": p.h1, "out2": p.out2, "attention": p.attention.view(p.n_cand, -1)},
     }[p.config_id]()
+
+
+def prepare_dca_layer(w, device="cuda"):
+    """Upload a `dca_layer_case` once: inputs and weights to HBM (K and V
+    weights of each group stacked so both come out of one GEMM)."""
+    dev = torch.device(device)
+    b = lambda a: _bf16(a, dev)   # noqa: E731
+    return SimpleNamespace(
+        r=w.n_req, n=w.n_cand, t=w.q_len, h=w.heads, d=w.head_dim,
+        co=_i32(w.cand_offsets, dev), ko=_i32(w.kv_offsets, dev),
+        y_req=b(w.y_req), y_cand=b(w.y_cand), s=b(w.s),
+        lcb_rr=b(w.lcb_rr), lcb_cr=b(w.lcb_cr), lcb_cc=b(w.lcb_cc),
+        w1_rr=b(w.w1_rr), w1_cr=b(w.w1_cr), w1_cc=b(w.w1_cc),
+        b1_r=_f32(w.b1_r, dev), b1_c=_f32(w.b1_c, dev),
+        w2_rr=b(w.w2_rr), w2_cr=b(w.w2_cr), w2_cc=b(w.w2_cc),
+        wkv_r=b(np.concatenate([w.wk_r, w.wv_r])), wkv_c=b(np.concatenate([w.wk_c, w.wv_c])))
+
+
+def dca_layer_step(p):
+    """One full DCA layer (Section 3.2) on the GPU: the ROCSified query
+    generator (LCB, then a two-layer GLM MLP; Eq. dca-query), the request- and
+    candidate-side K/V projections (one GEMM each), and the two cross
+    attentions (A^R through the identity map, A^C through the candidate map;
+    Eq. dca-attention). Every arithmetic step runs in librocs."""
+    r, n, t, h, d = p.r, p.n, p.t, p.h, p.d
+    z_r, z_c = ops.ikbo_lcb(p.y_req, p.y_cand, p.lcb_cr, p.lcb_cc, p.co, w_rr=p.lcb_rr)
+    h_r, h_c = ops.glm_linear(z_r.view(r, -1), z_c.view(n, -1), p.w1_rr, p.w1_cr, p.w1_cc,
+                              p.co, b_req=p.b1_r, b_cand=p.b1_c, activation="relu")
+    q_r, q_c = ops.glm_linear(h_r, h_c, p.w2_rr, p.w2_cr, p.w2_cc, p.co)
+    k_r, v_r = _kv_views(ops.ikbo_linear(p.s, p.wkv_r), h, d)
+    k_c, v_c = _kv_views(ops.ikbo_linear(p.s, p.wkv_c), h, d)
+    a_r = ops.dca_request_attention(q_r.view(r, t, h, d), k_r, v_r, p.ko)
+    a_c = ops.dca_attention(q_c.view(n, t, h, d), k_c, v_c, p.co, p.ko)
+    return {"q_req": q_r.view(r, t, h, d), "q_cand": q_c.view(n, t, h, d), "a_req": a_r,
+            "a_cand": a_c}
+
+
+def dca_layer(w, device="cuda"):
+    """prepare_dca_layer then one dca_layer_step."""
+    return dca_layer_step(prepare_dca_layer(w, device))

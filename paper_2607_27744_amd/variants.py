@@ -23,6 +23,10 @@ line with the call's algorithmic FLOPs and bytes against the MI355X peaks.
                     form on the same inputs
   glm_linear        the production-scale first layer as a full GLM layer
                     (request output 2048 -> 1024 as well)
+  dca_layer         a full DCA layer (Section 3.2): LCB + two-layer GLM MLP
+                    query generator, K/V projections for both groups, request-
+                    and candidate-side attention; 16 requests x 512 candidates,
+                    32 query tokens, 4 heads x 64, history 1024
 """
 
 import os
@@ -37,7 +41,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
 NAMES = ("lcb", "dca_tq32", "dca_tq64", "dca_request", "linear_mapped", "linear_combined",
-         "glm_linear")
+         "glm_linear", "dca_layer")
 
 
 def _bf16(a):
@@ -199,6 +203,26 @@ def _glm_linear(steps, warmup):
                                    + (2048 + 512) * 1024 + 1024 * 2048), "mfma", n, "candidates")
 
 
+def _dca_layer(steps, warmup):
+    from . import pipelines
+    r, n_r, length = 16, 512, 1024
+    kw = dict(f_req=64, f_cand=32, o_req=64, o_cand=32, emb=64, d_hidden=512, q_len=32,
+              heads=4, head_dim=64, d_seq=256)
+    w = wl.dca_layer_case([n_r] * r, [length] * r, seed=6, **kw)
+    p = pipelines.prepare_dca_layer(w)
+    ms = _time(lambda: pipelines.dca_layer_step(p), steps, warmup)
+    n, t, h, d = r * n_r, 32, 4, 64
+    d_r, d_c, d_q = 64 * 64, 32 * 64, t * h * d
+    flops = (2.0 * n * 32 * 32 * 64 + 2.0 * r * 96 * 64 * 64            # LCB
+             + 2.0 * n * d_c * 512 + 2.0 * r * (d_r * 512 * 2)            # MLP layer 1
+             + 2.0 * n * 512 * d_q + 2.0 * r * 512 * d_q * 2              # MLP layer 2
+             + 2.0 * 2 * r * length * 256 * 2 * h * d                     # K/V, both groups
+             + 4.0 * (n + r) * t * length * h * d)                        # attention
+    return _line("dca_layer", {"requests": r, "candidates": n, "q_len": t, "heads": h,
+                               "head_dim": d, "history": length, **kw},
+                 ms, flops, 0.0, "mfma", n, "candidates")
+
+
 def run(name, steps=20, warmup=3):
     """Time one variant; returns its JSON-ready record."""
     ops.load_library()
@@ -216,4 +240,6 @@ def run(name, steps=20, warmup=3):
         return _linear_combined(steps, warmup)
     if name == "glm_linear":
         return _glm_linear(steps, warmup)
+    if name == "dca_layer":
+        return _dca_layer(steps, warmup)
     raise ValueError(f"variant must be one of {NAMES}")

@@ -37,7 +37,8 @@ import torch
 
 __all__ = [
     "tensor_rng", "normal", "offsets_from_counts", "linear_case",
-    "attention_case", "fm_case", "lcb_case", "make_workload", "WORKLOAD_NAMES",
+    "attention_case", "fm_case", "lcb_case", "dca_layer_case", "make_workload",
+    "WORKLOAD_NAMES",
 ]
 
 WORKLOAD_NAMES = {
@@ -156,6 +157,39 @@ def lcb_case(counts, f_req, f_cand, o_req, o_cand, emb_dim, *, seed=0, config_id
                      bf16=bf16) if o_req else None),
         w_cr=np.ascontiguousarray(w[:, :f_req]), w_cc=np.ascontiguousarray(w[:, f_req:]),
         n_req=n_req, n_cand=n_cand,
+    )
+
+
+def dca_layer_case(counts, kv_lens, *, f_req=32, f_cand=16, o_req=32, o_cand=32, emb=64,
+                   d_hidden=256, q_len=8, heads=2, head_dim=64, d_seq=128, seed=0,
+                   config_id=500):
+    """One full DCA layer (Section 3.2): previous-layer GLM outputs y_req
+    [R, F_r, E] and y_cand [N, F_c, E], the shared sequence s [sum L_r, d_seq],
+    the query generator's weights (an LCB, then a two-layer GLM MLP whose
+    last layer emits q_len x heads x head_dim per group) and the request- and
+    candidate-side K/V projections, each [heads * head_dim, d_seq]."""
+    counts = np.asarray(counts, dtype=np.int64)
+    kv_lens = np.asarray(kv_lens, dtype=np.int64)
+    n_req, n_cand = counts.size, int(counts.sum())
+    d_r, d_c, d_q, hd = o_req * emb, o_cand * emb, q_len * heads * head_dim, heads * head_dim
+    g = lambda t, shape, fan: normal(tensor_rng(seed, config_id, t), shape,   # noqa: E731
+                                     std=1.0 / np.sqrt(fan))
+    return SimpleNamespace(
+        cand_offsets=offsets_from_counts(counts), kv_offsets=offsets_from_counts(kv_lens),
+        y_req=normal(tensor_rng(seed, config_id, 1), (n_req, f_req, emb)),
+        y_cand=normal(tensor_rng(seed, config_id, 2), (n_cand, f_cand, emb)),
+        s=normal(tensor_rng(seed, config_id, 3), (int(kv_lens.sum()), d_seq)),
+        lcb_rr=g(10, (o_req, f_req), f_req), lcb_cr=g(11, (o_cand, f_req), f_req + f_cand),
+        lcb_cc=g(12, (o_cand, f_cand), f_req + f_cand),
+        w1_rr=g(20, (d_hidden, d_r), d_r), w1_cr=g(21, (d_hidden, d_r), d_r + d_c),
+        w1_cc=g(22, (d_hidden, d_c), d_r + d_c),
+        b1_r=normal(tensor_rng(seed, config_id, 23), (d_hidden,), std=0.1, bf16=False),
+        b1_c=normal(tensor_rng(seed, config_id, 24), (d_hidden,), std=0.1, bf16=False),
+        w2_rr=g(30, (d_q, d_hidden), d_hidden), w2_cr=g(31, (d_q, d_hidden), 2 * d_hidden),
+        w2_cc=g(32, (d_q, d_hidden), 2 * d_hidden),
+        wk_r=g(40, (hd, d_seq), d_seq), wv_r=g(41, (hd, d_seq), d_seq),
+        wk_c=g(42, (hd, d_seq), d_seq), wv_c=g(43, (hd, d_seq), d_seq),
+        n_req=n_req, n_cand=n_cand, q_len=q_len, heads=heads, head_dim=head_dim,
     )
 
 

@@ -147,3 +147,26 @@ def test_workload_shapes_and_distributions(cid):
         assert w.w_req.shape == (512, 1024) and w.w_cand.shape == (512, 320)
     feats = w.e_c if cid == 3 else w.x_cand
     assert abs(float(np.mean(feats))) < 0.01 and abs(float(np.std(feats)) - 1) < 0.01
+
+
+def test_dca_layer_is_glm_compliant():
+    # Eq. glm-invariant for the whole DCA layer (query generator, K/V
+    # projections, both attentions): changing one candidate's input changes
+    # only that candidate's query and attention output, never a request-side
+    # output; and the request side equals single-request attention computed
+    # directly from its own queries.
+    w = wl.dca_layer_case([3, 0, 5, 2], [40, 9, 0, 17], seed=3)
+    base = pipelines.dca_layer(w)
+    w.y_cand = w.y_cand.copy()
+    w.y_cand[1] = -w.y_cand[1]              # candidate 1: request 0, history of 40
+    pert = pipelines.dca_layer(w)
+    for k in ("q_req", "a_req"):
+        np.testing.assert_array_equal(pert[k], base[k])
+    keep = np.arange(10) != 1
+    for k in ("q_cand", "a_cand"):
+        np.testing.assert_array_equal(pert[k][keep], base[k][keep])
+        assert not np.array_equal(pert[k][1], base[k][1])
+    # Candidates of request 2 (empty history) attend to nothing: zeros.
+    assert np.all(base["a_cand"][3:8] == 0.0)
+    # Request 2 has no history: its request-side attention is zero.
+    assert np.all(base["a_req"][2] == 0.0)
