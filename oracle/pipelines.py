@@ -41,6 +41,22 @@ def retrieval_mlp(w, rows=None):
     return {"h1": h1, "out": out}
 
 
+def ikbo_mlp2(x_req, x_cand, w1_req, w1_cand, b1, w2, b2, cand_offsets, act1="relu",
+              act2="none", rows=None):
+    """Two stacked GLM linear layers on the candidate group (Section 3.1,
+    closure under composition): H = act1(W1_CR x^R_{m_n} + W1_CC x^C_n + b1),
+    rounded onto the bf16 grid where the GPU keeps it (on chip, as the bf16
+    operand of the second product), then Y^C = act2(W2 H + b2).
+
+    The first layer is the broadcast form of Eq. glm-linear (x_req may be None
+    for a request-free first layer); the second has no request term.
+    Returns float64 [N, d_out] (or [len(rows), d_out]).
+    """
+    h = round_bf16(ikbo.ikbo_linear(x_req, x_cand, w1_req, w1_cand, b1, cand_offsets, act1,
+                                    rows=rows))
+    return ikbo.linear(h, w2, b2, act2)
+
+
 def _request_kv(s, wk, wv, kv_offsets, requests):
     """K = S W_K and V = S W_V for the listed requests only (others zero)."""
     k = np.zeros((s.shape[0], wk.shape[0]))

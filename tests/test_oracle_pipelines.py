@@ -170,3 +170,89 @@ def test_dca_layer_is_glm_compliant():
     assert np.all(base["a_cand"][3:8] == 0.0)
     # Request 2 has no history: its request-side attention is zero.
     assert np.all(base["a_req"][2] == 0.0)
+
+
+def _mlp2_case(counts, k_req=6, k_cand=5, d_hidden=8, d_out=3, seed=0):
+    rng = lambda t: wl.tensor_rng(seed, 55, t)  # noqa: E731
+    n_req, n = len(counts), int(np.sum(counts))
+    return SimpleNamespace(
+        cand_offsets=wl.offsets_from_counts(np.asarray(counts)),
+        x_req=wl.normal(rng(1), (n_req, k_req)), x_cand=wl.normal(rng(2), (n, k_cand)),
+        w1_req=wl.normal(rng(3), (d_hidden, k_req), std=0.4),
+        w1_cand=wl.normal(rng(4), (d_hidden, k_cand), std=0.4),
+        b1=wl.normal(rng(5), (d_hidden,), bf16=False),
+        w2=wl.normal(rng(6), (d_out, d_hidden), std=0.4),
+        b2=wl.normal(rng(7), (d_out,), bf16=False))
+
+
+def _mlp2(c, **kw):
+    return pipelines.ikbo_mlp2(c.x_req, c.x_cand, c.w1_req, c.w1_cand, c.b1, c.w2, c.b2,
+                               c.cand_offsets, **kw)
+
+
+def test_mlp2_index_probe_is_exact():
+    # x_req[r] = r everywhere, W1_CR picks feature 0 into hidden unit 0, the
+    # candidate weights are zero, W2 copies hidden unit 0: output column 0 is
+    # the owning request of every candidate, exactly (empty requests included).
+    counts = np.array([3, 0, 5, 1, 0, 4])
+    c = _mlp2_case(counts)
+    c.x_req = np.repeat(np.arange(6, dtype=np.float64)[:, None], 6, axis=1)
+    c.w1_req = np.zeros_like(c.w1_req)
+    c.w1_req[0, 0] = 1.0
+    c.w1_cand = np.zeros_like(c.w1_cand)
+    c.w2 = np.zeros_like(c.w2)
+    c.w2[0, 0] = 1.0
+    y = pipelines.ikbo_mlp2(c.x_req, c.x_cand, c.w1_req, c.w1_cand, None, c.w2, None,
+                            c.cand_offsets)
+    np.testing.assert_array_equal(y[:, 0], np.repeat(np.arange(6), counts))
+    np.testing.assert_array_equal(y[:, 1:], 0.0)
+
+
+def test_mlp2_rounds_the_hidden_layer_to_bf16():
+    # H = 1 + 2^-9 is below half the bf16 spacing at 1 (2^-7), so the hidden
+    # value the second layer sees is exactly 1: Y = 4, not 4 + 2^-7.
+    x_cand = np.array([[1.0, 2.0 ** -9]])
+    w1c, w2 = np.array([[1.0, 1.0]]), np.array([[4.0], [-4.0]])
+    y = pipelines.ikbo_mlp2(None, x_cand, None, w1c, None, w2, None, None, act1="none")
+    np.testing.assert_array_equal(y, [[4.0, -4.0]])
+    y = pipelines.ikbo_mlp2(None, x_cand, None, w1c, None, w2, None, None, act1="none",
+                            act2="relu")
+    np.testing.assert_array_equal(y, [[4.0, 0.0]])
+    # ReLU on the hidden layer: a negative pre-activation contributes nothing.
+    y = pipelines.ikbo_mlp2(None, -x_cand, None, w1c, None, w2, np.array([0.5, 0.25]), None)
+    np.testing.assert_array_equal(y, [[0.5, 0.25]])
+
+
+def test_mlp2_is_glm_compliant_and_matches_the_decomposed_layer():
+    counts = [3, 0, 5, 2]
+    c = _mlp2_case(counts)
+    base = _mlp2(c)
+    # The first layer by the Section 4.1 decomposition gives the same result.
+    h = round_bf16(ikbo.ikbo_linear_decomposed(c.x_req, c.x_cand, c.w1_req, c.w1_cand, c.b1,
+                                               c.cand_offsets, "relu"))
+    np.testing.assert_allclose(ikbo.linear(h, c.w2, c.b2), base, rtol=1e-12, atol=1e-12)
+    # Closure under composition: a candidate's input moves only its own row,
+    # a request's input moves exactly that request's candidates.
+    x2 = c.x_cand.copy()
+    x2[4] = -x2[4]
+    pert = pipelines.ikbo_mlp2(c.x_req, x2, c.w1_req, c.w1_cand, c.b1, c.w2, c.b2,
+                               c.cand_offsets)
+    keep = np.arange(10) != 4
+    np.testing.assert_array_equal(pert[keep], base[keep])
+    assert not np.array_equal(pert[4], base[4])
+    xr = c.x_req.copy()
+    xr[2] = xr[2] + 1.0
+    pert = pipelines.ikbo_mlp2(xr, c.x_cand, c.w1_req, c.w1_cand, c.b1, c.w2, c.b2,
+                               c.cand_offsets)
+    own = np.isin(np.arange(10), np.arange(3, 8))
+    np.testing.assert_array_equal(pert[~own], base[~own])
+    assert not np.array_equal(pert[own], base[own])
+    # Two candidates of one request with equal inputs get equal outputs (Eq. glm-sharing).
+    x3 = c.x_cand.copy()
+    x3[6] = x3[5]
+    same = pipelines.ikbo_mlp2(c.x_req, x3, c.w1_req, c.w1_cand, c.b1, c.w2, c.b2,
+                               c.cand_offsets)
+    np.testing.assert_array_equal(same[6], same[5])
+    # A row subset is the same rows of the full result.
+    rows = np.array([9, 0, 4])
+    np.testing.assert_array_equal(_mlp2(c, rows=rows), base[rows])
