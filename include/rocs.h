@@ -323,6 +323,51 @@ int32_t rocs_ikbo_lcb_mapped(const void* x_req, const void* x_cand,
 
 /*
  * ---------------------------------------------------------------------------
+ * rocs_ikbo_mlp2: two stacked GLM linear layers on the candidate group, the
+ * first with the request broadcast (Eq. glm-linear; a composition of
+ * GLM-compliant layers stays compliant, Section 3.1):
+ *
+ *   H[n]   = act1(W1_CR x^R_{m_n} + W1_CC x^C_n + b1)     [d_hidden]
+ *   out[n] = act2(W2 H[n] + b2)                           [d_out]
+ *
+ * H is rounded to the storage dtype before the second product (bf16: RNE),
+ * the same rounding as two separate rocs_ikbo_linear calls. IKBO form: the
+ * request table Zb = x_req W1_CR^T + b1 (fp32, workspace) is formed once per
+ * request; the fused candidate kernel keeps H on chip (no HBM round trip).
+ *
+ *   x_req   [R, k_req] (k_req may be 0: no request term; then x_req, w1_req
+ *           and cand_offsets are not read)
+ *   x_cand  [N, k_cand]
+ *   w1_req  [d_hidden, k_req]      w1_cand [d_hidden, k_cand]    b1 [d_hidden] or NULL
+ *   w2      [d_out, d_hidden]      b2 [d_out] or NULL
+ *   cand_offsets [R + 1] CSR (validate with rocs_validate_offsets if untrusted)
+ *   activation1, activation2: ROCS_ACT_NONE or ROCS_ACT_RELU
+ *   out     [N, d_out], not overlapping any input or the workspace
+ *   workspace  at least rocs_ikbo_mlp2_workspace_size(R, N, k_req, k_cand,
+ *              d_hidden, d_out, dtype) bytes, 256-byte aligned; scratch on
+ *              return. The size covers Zb, and for shapes without the fused
+ *              kernel also H [N, d_hidden] and the index map.
+ *
+ * Fused kernel: bf16, k_cand in {128, 256}, d_out in {128, 256}, d_hidden a
+ * multiple of 64 up to 1024, k_req a multiple of 8; it needs every pointer
+ * 16-byte aligned (ROCS_ERR_INVALID_ARGUMENT otherwise). Other shapes and
+ * fp32 run two launches of the linear kernels with H in the workspace.
+ * ---------------------------------------------------------------------------
+ */
+size_t rocs_ikbo_mlp2_workspace_size(int64_t num_requests, int64_t num_cand, int64_t k_req,
+                                     int64_t k_cand, int64_t d_hidden, int64_t d_out,
+                                     int32_t dtype);
+
+int32_t rocs_ikbo_mlp2(const void* x_req, int64_t k_req, const void* x_cand, int64_t k_cand,
+                       const void* w1_req, const void* w1_cand, const float* b1,
+                       const void* w2, const float* b2, const int32_t* cand_offsets,
+                       int64_t num_requests, int64_t num_cand, int64_t d_hidden,
+                       int64_t d_out, int32_t dtype, int32_t activation1,
+                       int32_t activation2, void* out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * Index-map helpers (Section 4.1, m in {0..B_r-1}^{B_c}).
  *
  * rocs_request_ids: out_ids[n] = m_n for n < N, computed on the device by the

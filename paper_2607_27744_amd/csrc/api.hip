@@ -460,6 +460,123 @@ int32_t rocs_ikbo_lcb_mapped(const void* x_req, const void* x_cand, const void* 
                   y_cand, workspace, workspace_bytes, stream);
 }
 
+// The fused two-layer kernel's shapes (bf16). Other shapes and fp32 run the
+// two-launch form, which keeps H in the workspace.
+static bool mlp2_fused(int64_t k_req, int64_t k_cand, int64_t d_hidden, int64_t d_out,
+                       int32_t dtype) {
+  return dtype == ROCS_DTYPE_BF16 && k_req % 8 == 0 &&
+         rocs::mlp2_fused_shape(k_cand, d_hidden, d_out);
+}
+
+size_t rocs_ikbo_mlp2_workspace_size(int64_t num_requests, int64_t num_cand, int64_t k_req,
+                                     int64_t k_cand, int64_t d_hidden, int64_t d_out,
+                                     int32_t dtype) {
+  if (num_requests < 0 || num_cand <= 0 || k_req < 0 || k_cand < 1 || d_hidden < 1 ||
+      d_out < 1 || !valid_dtype(dtype))
+    return 0;
+  size_t n = 0;
+  const bool req = k_req > 0 && num_requests > 0;
+  // Request table Zb [R, d_hidden] fp32.
+  if (req) n += align256((size_t)num_requests * (size_t)d_hidden * sizeof(float));
+  if (!mlp2_fused(k_req, k_cand, d_hidden, d_out, dtype)) {
+    if (req) n += align256((size_t)num_cand * sizeof(int32_t));   // index map
+    n += align256((size_t)num_cand * (size_t)d_hidden * esize(dtype));   // H
+  }
+  return n;
+}
+
+int32_t rocs_ikbo_mlp2(const void* x_req, int64_t k_req, const void* x_cand, int64_t k_cand,
+                       const void* w1_req, const void* w1_cand, const float* b1,
+                       const void* w2, const float* b2, const int32_t* cand_offsets,
+                       int64_t R, int64_t N, int64_t d_hidden, int64_t d_out, int32_t dtype,
+                       int32_t activation1, int32_t activation2, void* out, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  for (int32_t act : {activation1, activation2})
+    if (act != ROCS_ACT_NONE && act != ROCS_ACT_RELU)
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown activation %d", act);
+  if (R < 0 || N < 0 || k_req < 0 || k_cand < 1 || d_hidden < 1 || d_out < 1)
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "sizes must satisfy R >= 0, N >= 0, k_req >= 0, k_cand >= 1, d_hidden >= 1, "
+                "d_out >= 1");
+  if (R > kMaxI32 || N > kMaxI32 || k_req > kMaxI32 || k_cand > kMaxI32 ||
+      d_hidden > kMaxI32 || d_out > kMaxI32)
+    return fail(ROCS_ERR_UNSUPPORTED, "a size exceeds 2^31 - 1");
+  if (N == 0) return ok();
+  if (k_req > 0 && R == 0)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests to own them");
+  if (x_cand == nullptr || w1_cand == nullptr || w2 == nullptr || out == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "x_cand, w1_cand, w2 and out must not be NULL");
+  if (k_req > 0 && (x_req == nullptr || w1_req == nullptr || cand_offsets == nullptr))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "k_req > 0 needs x_req, w1_req and cand_offsets");
+  const bool fused = mlp2_fused(k_req, k_cand, d_hidden, d_out, dtype);
+  if (fused && !(aligned(x_cand, 16) && aligned(w1_cand, 16) && aligned(w2, 16) &&
+                 aligned(out, 16) && aligned(b1, 16) && aligned(b2, 16) &&
+                 aligned(x_req, 16) && aligned(w1_req, 16)))
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "the fused kernel needs 16-byte aligned x_req, x_cand, w1_req, w1_cand, b1, "
+                "w2, b2 and out");
+  const size_t need = rocs_ikbo_mlp2_workspace_size(R, N, k_req, k_cand, d_hidden, d_out, dtype);
+  if (need > 0) {
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(ROCS_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need,
+                  workspace == nullptr ? (size_t)0 : workspace_bytes);
+    if (!aligned(workspace, 256))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  }
+  const size_t es = esize(dtype);
+  const size_t out_bytes = (size_t)N * d_out * es;
+  const struct { const void* p; size_t n; const char* name; } ins[] = {
+      {x_req, (size_t)R * k_req * es, "x_req"},
+      {x_cand, (size_t)N * k_cand * es, "x_cand"},
+      {w1_req, (size_t)d_hidden * k_req * es, "w1_req"},
+      {w1_cand, (size_t)d_hidden * k_cand * es, "w1_cand"},
+      {b1, (size_t)d_hidden * sizeof(float), "b1"},
+      {w2, (size_t)d_out * d_hidden * es, "w2"},
+      {b2, (size_t)d_out * sizeof(float), "b2"},
+      {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"},
+  };
+  for (const auto& in : ins) {
+    if (overlap(out, out_bytes, in.p, in.n))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "out overlaps %s", in.name);
+    if (need > 0 && overlap(workspace, need, in.p, in.n))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace overlaps %s", in.name);
+  }
+  if (need > 0 && overlap(workspace, need, out, out_bytes))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace overlaps out");
+  // One workgroup per 128-candidate tile slot.
+  if (R + N / 128 + 1 >= kMaxI32) return fail(ROCS_ERR_UNSUPPORTED, "batch too large");
+
+  rocs::Mlp2Args a{};
+  a.x_req = x_req; a.x_cand = x_cand; a.cand_offsets = cand_offsets;
+  a.w1_req = w1_req; a.w1_cand = w1_cand; a.b1 = b1; a.w2 = w2; a.b2 = b2;
+  a.R = R; a.N = N; a.k_req = k_req; a.k_cand = k_cand; a.d_hidden = d_hidden; a.d_out = d_out;
+  a.bf16 = dtype == ROCS_DTYPE_BF16;
+  a.relu1 = activation1 == ROCS_ACT_RELU;
+  a.relu2 = activation2 == ROCS_ACT_RELU;
+  a.out = out;
+  char* ws = static_cast<char*>(workspace);
+  size_t at = 0;
+  if (k_req > 0) {
+    a.z = reinterpret_cast<float*>(ws);
+    at = align256((size_t)R * d_hidden * sizeof(float));
+  }
+  if (!fused) {
+    if (k_req > 0) {
+      a.ids = reinterpret_cast<int32_t*>(ws + at);
+      at += align256((size_t)N * sizeof(int32_t));
+    }
+    a.h = ws + at;
+    a.linear_fast = a.bf16 && k_cand % 8 == 0 && k_req % 8 == 0 && d_hidden % 8 == 0 &&
+                    d_out % 4 == 0 && aligned(x_cand, 16) && aligned(w1_cand, 16) &&
+                    aligned(x_req, 16) && aligned(w1_req, 16) && aligned(b1, 16) &&
+                    aligned(w2, 16) && aligned(b2, 16) && aligned(out, 16);
+  }
+  const hipError_t e = rocs::launch_mlp2(a, fused, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_ikbo_mlp2: %s", hipGetErrorString(e));
+  return ok();
+}
+
 int32_t rocs_request_ids(const int32_t* cand_offsets, int64_t R, int64_t N, int32_t* out_ids,
                          void* stream) {
   if (R < 0 || N < 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "negative size");

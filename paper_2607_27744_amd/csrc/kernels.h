@@ -70,6 +70,24 @@ struct LcbArgs {
   float* z;             // [R, o_cand, emb] workspace
 };
 
+struct Mlp2Args {
+  const void* x_req;    // [R, k_req]
+  const void* x_cand;   // [N, k_cand]
+  const int32_t* cand_offsets;   // CSR [R + 1] (k_req > 0)
+  const void* w1_req;   // [d_hidden, k_req]
+  const void* w1_cand;  // [d_hidden, k_cand]
+  const float* b1;      // [d_hidden] or NULL
+  const void* w2;       // [d_out, d_hidden]
+  const float* b2;      // [d_out] or NULL
+  int64_t R, N, k_req, k_cand, d_hidden, d_out;
+  bool bf16, relu1, relu2;
+  bool linear_fast;     // the two-launch form may take the fast linear kernels
+  void* out;            // [N, d_out]
+  float* z;             // [R, d_hidden] workspace (k_req > 0)
+  int32_t* ids;         // [N] workspace of the two-launch form (k_req > 0)
+  void* h;              // [N, d_hidden] workspace of the two-launch form
+};
+
 // Each returns hipSuccess or the launch error.
 hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t* ids,
                               hipStream_t s);
@@ -78,5 +96,9 @@ hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s);
 hipError_t launch_interaction(const InteractionArgs& a, bool fast, hipStream_t s);
 hipError_t launch_lcb(const LcbArgs& a, bool fast, hipStream_t s);
 bool lcb_fast_shape(int f_cand, int o_cand, int emb);
+// The request table Zb = x_req W_req^T + bias (fp32, [R, d_out]) alone, bf16 in.
+hipError_t launch_request_table(const LinearArgs& a, hipStream_t s);
+hipError_t launch_mlp2(const Mlp2Args& a, bool fused, hipStream_t s);
+bool mlp2_fused_shape(int64_t k_cand, int64_t d_hidden, int64_t d_out);
 
 }  // namespace rocs

@@ -833,6 +833,16 @@ hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t*
                        off, (int)R, N, ids);
 }
 
+hipError_t launch_request_table(const LinearArgs& a, hipStream_t s) {
+  const int tiles_d = (int)((a.d_out + 15) / 16);
+  const int req_tiles = tiles_d * (int)((a.R + 15) / 16);
+  const RequestOut none{nullptr, nullptr, nullptr, 0, 0, 0};
+  return launch_kernel(request_gemm_bf16, dim3(req_tiles), dim3(256), s,
+                       static_cast<const bf16_t*>(a.x_req), static_cast<const bf16_t*>(a.w_req),
+                       a.bias, a.z, a.cand_offsets, a.ids, (int)a.R, a.N, (int)a.k_req,
+                       (int)a.d_out, tiles_d, req_tiles, none);
+}
+
 hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
   if (!fast) {
     if (a.y_req != nullptr) {

@@ -16,7 +16,8 @@ from . import _lib
 __all__ = [
     "load_library", "ikbo_linear", "ikbo_linear_mapped", "glm_linear", "linear_workspace_size",
     "dca_attention", "dca_attention_mapped", "dca_request_attention", "glm_interaction",
-    "ikbo_lcb", "ikbo_lcb_mapped", "request_ids", "validate_offsets", "RocsError",
+    "ikbo_lcb", "ikbo_lcb_mapped", "ikbo_mlp2", "mlp2_workspace_size", "request_ids",
+    "validate_offsets", "RocsError",
 ]
 
 RocsError = _lib.RocsError
@@ -174,6 +175,65 @@ def _linear(x_cand, w_cand, x_req, w_req, cand_offsets, cand_ids, mapped, bias, 
         _ptr(x_req), k_req, _ptr(x_cand), _ptr(x_cand_add), k_cand, _ptr(w_req), _ptr(w_cand),
         _ptr(bias), _ptr(index), n_req, n_cand, d_out, code, _ACT[activation],
         _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)), name)
+    return out
+
+
+def mlp2_workspace_size(num_requests, num_cand, k_req, k_cand, d_hidden, d_out, dtype):
+    code = _lib.DTYPE_BF16 if dtype == torch.bfloat16 else _lib.DTYPE_F32
+    return int(_lib.load().rocs_ikbo_mlp2_workspace_size(num_requests, num_cand, k_req, k_cand,
+                                                          d_hidden, d_out, code))
+
+
+def ikbo_mlp2(x_cand, w1_cand, w2, *, x_req=None, w1_req=None, cand_offsets=None, b1=None,
+              b2=None, activation1="relu", activation2="none", out=None, workspace=None,
+              stream=None):
+    """rocs_ikbo_mlp2: out[n] = act2(w2 @ H[n] + b2), H[n] = act1(w1_cand @ x_cand[n] +
+    w1_req @ x_req[m_n] + b1) rounded to the input dtype; H stays on chip on the fused path.
+
+    x_cand [N, K_c], w1_cand [D_h, K_c], w2 [D_o, D_h], x_req [R, K_r], w1_req [D_h, K_r],
+    cand_offsets [R + 1] int32, b1 [D_h] and b2 [D_o] float32.
+    """
+    lib = _lib.load()
+    _need(x_cand.dim() == 2 and w1_cand.dim() == 2 and w2.dim() == 2, "2-D operands expected")
+    n_cand, k_cand = x_cand.shape
+    d_hidden = w1_cand.shape[0]
+    _need(w1_cand.shape[1] == k_cand, "w1_cand must be [d_hidden, k_cand]")
+    _need(w2.shape[1] == d_hidden, "w2 must be [d_out, d_hidden]")
+    d_out = w2.shape[0]
+    code = _dtype_code(x_cand)
+    for t in (w1_cand, w2, x_req, w1_req):
+        _need(t is None or t.dtype == x_cand.dtype, "inputs must share one dtype")
+    if x_req is not None:
+        _need(w1_req is not None and cand_offsets is not None,
+              "x_req needs w1_req and cand_offsets")
+        _need(x_req.dim() == 2 and w1_req.dim() == 2, "x_req and w1_req must be 2-D")
+        n_req, k_req = x_req.shape
+        _need(w1_req.shape == (d_hidden, k_req), "w1_req must be [d_hidden, k_req]")
+        _offsets(cand_offsets, n_req)
+    else:
+        n_req, k_req = 0, 0
+    for b, n, name in ((b1, d_hidden, "b1"), (b2, d_out, "b2")):
+        if b is not None:
+            _need(b.dtype == torch.float32 and b.shape == (n,), f"{name} must be float32 [{n}]")
+    for t in (x_cand, w1_cand, w2, x_req, w1_req, b1, b2):
+        _need(t is None or t.is_contiguous(), "tensors must be contiguous")
+    if out is None:
+        out = torch.empty((n_cand, d_out), dtype=x_cand.dtype, device=x_cand.device)
+    _need(out.shape == (n_cand, d_out) and out.dtype == x_cand.dtype and out.is_contiguous(),
+          "out must be a contiguous [N, d_out] tensor of the input dtype")
+    need = int(lib.rocs_ikbo_mlp2_workspace_size(n_req, n_cand, k_req, k_cand, d_hidden, d_out,
+                                                 code))
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x_cand.device)
+    _on_gpu(x_cand, w1_cand, w2, x_req, w1_req, cand_offsets, b1, b2, out, workspace)
+    for a in (activation1, activation2):
+        _need(a in _ACT, f"activation must be one of {sorted(k for k in _ACT if k)}")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _lib.check(lib.rocs_ikbo_mlp2(
+        _ptr(x_req), k_req, _ptr(x_cand), k_cand, _ptr(w1_req), _ptr(w1_cand), _ptr(b1), _ptr(w2),
+        _ptr(b2), _ptr(cand_offsets), n_req, n_cand, d_hidden, d_out, code, _ACT[activation1],
+        _ACT[activation2], _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)),
+        "rocs_ikbo_mlp2")
     return out
 
 

@@ -27,6 +27,9 @@ line with the call's algorithmic FLOPs and bytes against the MI355X peaks.
                     query generator, K/V projections for both groups, request-
                     and candidate-side attention; 16 requests x 512 candidates,
                     32 query tokens, 4 heads x 64, history 1024
+  mlp2              the retrieval MLP (64 requests, ~65k candidates, 1024+256
+                    -> 512 ReLU -> 256) as one fused call with the hidden
+                    layer on chip, timed beside the two linear launches
 """
 
 import os
@@ -41,7 +44,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
 NAMES = ("lcb", "dca_tq32", "dca_tq64", "dca_request", "linear_mapped", "linear_combined",
-         "glm_linear", "dca_layer")
+         "glm_linear", "dca_layer", "mlp2")
 
 
 def _bf16(a):
@@ -223,6 +226,33 @@ def _dca_layer(steps, warmup):
                  ms, flops, 0.0, "mfma", n, "candidates")
 
 
+def _mlp2(steps, warmup):
+    w = wl.make_workload(2, seed=0)
+    n = w.n_cand
+    xc, w1c, w2 = _bf16(w.x_cand), _bf16(w.w1_cand), _bf16(w.w2)
+    kw = dict(x_req=_bf16(w.x_req), w1_req=_bf16(w.w1_req), cand_offsets=_i32(w.cand_offsets))
+    out = torch.empty((n, 256), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(ops.mlp2_workspace_size(64, n, 1024, 256, 512, 256, torch.bfloat16),
+                     dtype=torch.uint8, device="cuda")
+    ms = _time(lambda: ops.ikbo_mlp2(xc, w1c, w2, out=out, workspace=ws, **kw), steps, warmup)
+    # The same two layers as two linear launches (H through HBM).
+    h = torch.empty((n, 512), dtype=torch.bfloat16, device="cuda")
+    lws = torch.empty(ops.linear_workspace_size(64, n, 512, 1024), dtype=torch.uint8,
+                      device="cuda")
+    w1r, co, xr = kw["w1_req"], kw["cand_offsets"], kw["x_req"]
+
+    def two():
+        ops.ikbo_linear(xc, w1c, x_req=xr, w_req=w1r, cand_offsets=co, activation="relu", out=h,
+                        workspace=lws)
+        ops.ikbo_linear(h, w2, out=out)
+    ms_two = _time(two, steps, warmup)
+    flops = 2.0 * n * (256 * 512 + 512 * 256) + 2.0 * 64 * 1024 * 512
+    byts = 2.0 * (n * 256 + n * 256 + 64 * 1024 + 1280 * 512 + 512 * 256)
+    return _line("mlp2", {"requests": 64, "candidates": n, "k_req": 1024, "k_cand": 256,
+                          "d_hidden": 512, "d_out": 256},
+                 ms, flops, byts, "mfma", n, "candidates", {"two_launch_ms": round(ms_two, 4)})
+
+
 def run(name, steps=20, warmup=3):
     """Time one variant; returns its JSON-ready record."""
     ops.load_library()
@@ -242,4 +272,6 @@ def run(name, steps=20, warmup=3):
         return _glm_linear(steps, warmup)
     if name == "dca_layer":
         return _dca_layer(steps, warmup)
+    if name == "mlp2":
+        return _mlp2(steps, warmup)
     raise ValueError(f"variant must be one of {NAMES}")

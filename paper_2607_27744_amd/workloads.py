@@ -160,6 +160,32 @@ def lcb_case(counts, f_req, f_cand, o_req, o_cand, emb_dim, *, seed=0, config_id
     )
 
 
+def mlp2_case(counts, k_req, k_cand, d_hidden, d_out, *, seed=0, config_id=600, bf16=True,
+              biases=True):
+    """Two stacked linear layers, the first with a request term: x_req [R, K_r],
+    x_cand [N, K_c], [w1_req | w1_cand] drawn as one [D_h, K_r + K_c] matrix
+    with std 1/sqrt(K_r + K_c), w2 [D_o, D_h] with std 1/sqrt(D_h), and float32
+    biases b1 [D_h], b2 [D_o] with std 0.1 (None without biases)."""
+    counts = np.asarray(counts, dtype=np.int64)
+    n_req, n_cand = counts.size, int(counts.sum())
+    fan = k_req + k_cand
+    w1 = normal(tensor_rng(seed, config_id, 3), (d_hidden, fan), std=1.0 / np.sqrt(fan),
+                bf16=bf16)
+    return SimpleNamespace(
+        cand_offsets=offsets_from_counts(counts),
+        x_req=normal(tensor_rng(seed, config_id, 1), (n_req, k_req), bf16=bf16),
+        x_cand=normal(tensor_rng(seed, config_id, 2), (n_cand, k_cand), bf16=bf16),
+        w1_req=np.ascontiguousarray(w1[:, :k_req]), w1_cand=np.ascontiguousarray(w1[:, k_req:]),
+        w2=normal(tensor_rng(seed, config_id, 4), (d_out, d_hidden), std=1.0 / np.sqrt(d_hidden),
+                  bf16=bf16),
+        b1=(normal(tensor_rng(seed, config_id, 5), (d_hidden,), std=0.1, bf16=False)
+            if biases else None),
+        b2=(normal(tensor_rng(seed, config_id, 6), (d_out,), std=0.1, bf16=False)
+            if biases else None),
+        n_req=n_req, n_cand=n_cand,
+    )
+
+
 def dca_layer_case(counts, kv_lens, *, f_req=32, f_cand=16, o_req=32, o_cand=32, emb=64,
                    d_hidden=256, q_len=8, heads=2, head_dim=64, d_seq=128, seed=0,
                    config_id=500):

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 15
+    assert len(names) == 17
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -171,6 +171,38 @@ def test_lcb_argument_errors(lib):
     assert call(yc=FAKE[1]) == _lib.INVALID_ARGUMENT              # y_cand aliases x_cand
     assert call(R=0) == _lib.INVALID_ARGUMENT                     # candidates without requests
     assert call(R=0, N=0) == _lib.OK
+
+
+@no_gpu
+def test_mlp2_argument_errors(lib):
+    # Every call below fails validation (or has nothing to do) before any launch.
+    def call(**kw):
+        a = dict(xr=FAKE[0], kr=8, xc=FAKE[1], kc=128, w1r=FAKE[2], w1c=FAKE[3], b1=None,
+                 w2=FAKE[4], b2=None, co=FAKE[5], R=2, N=16, dh=64, do=128, dtype=1, a1=1, a2=0,
+                 out=FAKE[6], ws=FAKE[7], ws_bytes=64, stream=None)
+        a.update(kw)
+        return lib.rocs_ikbo_mlp2(*a.values())
+    size = lib.rocs_ikbo_mlp2_workspace_size
+    assert size(2, 16, 8, 128, 64, 128, 1) == 512                 # Zb only (fused shape)
+    assert size(2, 16, 8, 8, 64, 128, 1) == 512 + 256 + 2048       # + index map + H
+    assert size(2, 16, 0, 128, 64, 128, 1) == 0                    # fused, no request term
+    assert size(2, 16, 8, 128, 64, 128, 0) == 512 + 256 + 4096     # fp32: two launches
+    assert size(2, 0, 8, 128, 64, 128, 1) == 0
+    assert call(dtype=7) == _lib.INVALID_ARGUMENT
+    assert call(a1=3) == _lib.INVALID_ARGUMENT
+    assert call(a2=-1) == _lib.INVALID_ARGUMENT
+    assert call(kc=0) == _lib.INVALID_ARGUMENT
+    assert call(xc=None) == _lib.INVALID_ARGUMENT
+    assert call(w2=None) == _lib.INVALID_ARGUMENT
+    assert call(co=None) == _lib.INVALID_ARGUMENT
+    assert call(R=0) == _lib.INVALID_ARGUMENT                      # candidates without requests
+    assert call(xc=P(0x20008)) == _lib.INVALID_ARGUMENT            # fused kernel: misaligned
+    assert call() == _lib.WORKSPACE_TOO_SMALL                      # 64 < 512 bytes
+    assert call(ws=None) == _lib.WORKSPACE_TOO_SMALL
+    assert call(ws_bytes=1 << 20, ws=P(0x80010)) == _lib.INVALID_ARGUMENT   # not 256-aligned
+    assert call(ws_bytes=1 << 20, out=FAKE[1]) == _lib.INVALID_ARGUMENT     # out aliases x_cand
+    assert call(ws_bytes=1 << 20, ws=FAKE[3]) == _lib.INVALID_ARGUMENT      # ws aliases w1_cand
+    assert call(N=0) == _lib.OK
 
 
 @no_gpu
