@@ -42,18 +42,20 @@ def retrieval_mlp(w, rows=None):
 
 
 def ikbo_mlp2(x_req, x_cand, w1_req, w1_cand, b1, w2, b2, cand_offsets, act1="relu",
-              act2="none", rows=None):
+              act2="none", rows=None, hidden="bf16"):
     """Two stacked GLM linear layers on the candidate group (Section 3.1,
     closure under composition): H = act1(W1_CR x^R_{m_n} + W1_CC x^C_n + b1),
     rounded onto the bf16 grid where the GPU keeps it (on chip, as the bf16
-    operand of the second product), then Y^C = act2(W2 H + b2).
+    operand of the second product; hidden="f32" leaves it unrounded, as an
+    fp32 pipeline stores it), then Y^C = act2(W2 H + b2).
 
     The first layer is the broadcast form of Eq. glm-linear (x_req may be None
     for a request-free first layer); the second has no request term.
     Returns float64 [N, d_out] (or [len(rows), d_out]).
     """
-    h = round_bf16(ikbo.ikbo_linear(x_req, x_cand, w1_req, w1_cand, b1, cand_offsets, act1,
-                                    rows=rows))
+    h = ikbo.ikbo_linear(x_req, x_cand, w1_req, w1_cand, b1, cand_offsets, act1, rows=rows)
+    if hidden == "bf16":
+        h = round_bf16(h)
     return ikbo.linear(h, w2, b2, act2)
 
 
@@ -101,18 +103,30 @@ def _attend_rows(q_rows, k, v, w, sel, h, d):  # noqa: D401
     return o.reshape(sel.size, h * d)
 
 
+def glm_fm_linear(x_req, x_cand, w_req, w_cand, bias, cand_offsets, act="relu", rows=None):
+    """A GLM FM interaction feeding a GLM linear (Section 3.1, closure under
+    composition): Y^R, Y^C = FM(X^R, X^C) (Eq. glm-fm-two-groups, flattened),
+    both rounded onto the bf16 grid where the GPU hands them on, then
+    out = act(W_CR Y^R_{m_n} + W_CC Y^C_n + b) (Eq. glm-linear).
+    Returns float64 (y_req [R, F_r^2], y_cand [N or len(rows), F_c (F_r + F_c)],
+    out [N or len(rows), D]); out is not rounded."""
+    y_req, y_cand = ikbo.glm_fm(x_req, x_cand, cand_offsets, rows=rows)
+    y_req = round_bf16(y_req)
+    y_cand = round_bf16(y_cand)
+    sel = _rows_or_all(np.asarray(x_cand).shape[0], rows)
+    reqs = ikbo.request_ids(cand_offsets)[sel]
+    # The selected candidates as a one-request-per-candidate batch, so the
+    # linear sees exactly their own request rows.
+    out = ikbo.ikbo_linear(y_req[reqs], y_cand, w_req, w_cand, bias, np.arange(sel.size + 1),
+                           act)
+    return y_req, y_cand, out
+
+
 def fm_linear(w, rows=None):
     """Workload 4: GLM FM interaction, then an IKBO linear (ReLU) on
     x_req = Y^R [R, F_r^2] and x_cand = Y^C [N, F_c (F_r + F_c)]."""
-    y_req, y_cand = ikbo.glm_fm(w.x_req, w.x_cand, w.cand_offsets, rows=rows)
-    y_req = round_bf16(y_req)
-    y_cand = round_bf16(y_cand)
-    sel = _rows_or_all(w.n_cand, rows)
-    reqs = ikbo.request_ids(w.cand_offsets)[sel]
-    # The selected candidates as a one-request-per-candidate batch, so the
-    # linear sees exactly their own request rows.
-    out = ikbo.ikbo_linear(y_req[reqs], y_cand, w.w_req, w.w_cand, None,
-                           np.arange(sel.size + 1), "relu")
+    y_req, y_cand, out = glm_fm_linear(w.x_req, w.x_cand, w.w_req, w.w_cand, None,
+                                       w.cand_offsets, "relu", rows=rows)
     return {"y_req": y_req, "y_cand": y_cand, "out": round_bf16(out)}
 
 

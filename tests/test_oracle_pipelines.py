@@ -216,6 +216,9 @@ def test_mlp2_rounds_the_hidden_layer_to_bf16():
     y = pipelines.ikbo_mlp2(None, x_cand, None, w1c, None, w2, None, None, act1="none")
     np.testing.assert_array_equal(y, [[4.0, -4.0]])
     y = pipelines.ikbo_mlp2(None, x_cand, None, w1c, None, w2, None, None, act1="none",
+                            hidden="f32")
+    np.testing.assert_array_equal(y, [[4.0 + 2.0 ** -7, -4.0 - 2.0 ** -7]])
+    y = pipelines.ikbo_mlp2(None, x_cand, None, w1c, None, w2, None, None, act1="none",
                             act2="relu")
     np.testing.assert_array_equal(y, [[4.0, 0.0]])
     # ReLU on the hidden layer: a negative pre-activation contributes nothing.
@@ -256,3 +259,68 @@ def test_mlp2_is_glm_compliant_and_matches_the_decomposed_layer():
     # A row subset is the same rows of the full result.
     rows = np.array([9, 0, 4])
     np.testing.assert_array_equal(_mlp2(c, rows=rows), base[rows])
+
+
+def _fm_case(counts, f_r=4, f_c=2, e=8, d=5, seed=0):
+    rng = lambda t: wl.tensor_rng(seed, 66, t)  # noqa: E731
+    n_req, n = len(counts), int(np.sum(counts))
+    return SimpleNamespace(
+        cand_offsets=wl.offsets_from_counts(np.asarray(counts)),
+        x_req=wl.normal(rng(1), (n_req, f_r, e)), x_cand=wl.normal(rng(2), (n, f_c, e)),
+        w_req=wl.normal(rng(3), (d, f_r * f_r), std=0.3),
+        w_cand=wl.normal(rng(4), (d, f_c * (f_r + f_c)), std=0.3),
+        bias=wl.normal(rng(5), (d,), bf16=False))
+
+
+def test_fm_linear_probe_is_exact():
+    # One-hot embeddings make every interaction value 0 or 1: request r's
+    # fields are e_0 .. e_{F_r - 1} scaled by r, candidate field i is e_i.
+    # Y^R[r] = r^2 I, Y^C[n] = [r e_i . e_j | I]; with W_CR summing the
+    # diagonal and W_CC picking the request-candidate block's (0, 0) entry:
+    # out[n] = F_r r^2 + r, exact.
+    counts = [2, 0, 3, 1]
+    c = _fm_case(counts, f_r=4, f_c=2, e=8, d=2)
+    c.x_req = np.zeros_like(c.x_req)
+    for r in range(4):
+        c.x_req[r, :, :4] = r * np.eye(4)
+    c.x_cand = np.zeros_like(c.x_cand)
+    c.x_cand[:, 0, 0] = 1.0
+    c.x_cand[:, 1, 1] = 1.0
+    c.w_req = np.zeros_like(c.w_req)
+    c.w_req[0, [0, 5, 10, 15]] = 1.0                    # trace of Y^R
+    c.w_cand = np.zeros_like(c.w_cand)
+    c.w_cand[1, 0] = 1.0                                # Y^C[n][field 0][request field 0]
+    y_req, y_cand, out = pipelines.glm_fm_linear(c.x_req, c.x_cand, c.w_req, c.w_cand, None,
+                                                 c.cand_offsets, "none")
+    m = np.repeat(np.arange(4), counts)
+    np.testing.assert_array_equal(out[:, 0], 4.0 * m ** 2)
+    np.testing.assert_array_equal(out[:, 1], m)
+    # Y^C of candidate n: field 0 against the request fields is r e_0, and
+    # the candidate block is the 2 x 2 identity.
+    np.testing.assert_array_equal(y_cand[:, :6], np.stack([m, 0 * m, 0 * m, 0 * m, 1 + 0 * m,
+                                                            0 * m], axis=1))
+
+
+def test_fm_linear_is_glm_compliant():
+    counts = [3, 0, 4, 2]
+    c = _fm_case(counts)
+    _, _, base = pipelines.glm_fm_linear(c.x_req, c.x_cand, c.w_req, c.w_cand, c.bias,
+                                         c.cand_offsets, "none")
+    x2 = c.x_cand.copy()
+    x2[5] = -x2[5]
+    _, _, pert = pipelines.glm_fm_linear(c.x_req, x2, c.w_req, c.w_cand, c.bias,
+                                         c.cand_offsets, "none")
+    keep = np.arange(9) != 5
+    np.testing.assert_array_equal(pert[keep], base[keep])
+    assert not np.array_equal(pert[5], base[5])
+    xr = c.x_req.copy()
+    xr[3] = 2.0 * xr[3]
+    _, _, pert = pipelines.glm_fm_linear(xr, c.x_cand, c.w_req, c.w_cand, c.bias,
+                                         c.cand_offsets, "none")
+    own = np.arange(9) >= 7
+    np.testing.assert_array_equal(pert[~own], base[~own])
+    assert not np.array_equal(pert[own], base[own])
+    rows = np.array([8, 0, 4])
+    _, yc, sub = pipelines.glm_fm_linear(c.x_req, c.x_cand, c.w_req, c.w_cand, c.bias,
+                                         c.cand_offsets, "none", rows=rows)
+    np.testing.assert_array_equal(sub, base[rows])
