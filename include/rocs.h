@@ -368,6 +368,49 @@ int32_t rocs_ikbo_mlp2(const void* x_req, int64_t k_req, const void* x_cand, int
 
 /*
  * ---------------------------------------------------------------------------
+ * rocs_glm_fm_linear: a GLM FM interaction (Eq. glm-fm-two-groups, flattened
+ * as in rocs_glm_interaction) feeding a GLM linear (Eq. glm-linear); the
+ * composition stays GLM-compliant (Section 3.1):
+ *
+ *   Y^R_r  = X^R_r (X^R_r)^T                                     [f_req^2]
+ *   Y^C_n  = [X^C_n (X^R_{m_n})^T | X^C_n (X^C_n)^T]              [f_cand (f_req + f_cand)]
+ *   out[n] = act(W_CR Y^R_{m_n} + W_CC Y^C_n + bias)             [d_out]
+ *
+ * Y^R and Y^C are rounded to the storage dtype before the linear (bf16:
+ * RNE), the same rounding as rocs_glm_interaction followed by
+ * rocs_ikbo_linear. IKBO form: Y^R and Zb = W_CR Y^R + bias (fp32) are formed
+ * once per request in the workspace; the fused candidate kernel computes Y^C
+ * in registers as the linear's operand, so Y^C never reaches HBM.
+ *
+ *   x_req  [R, f_req, emb_dim]       x_cand [N, f_cand, emb_dim]
+ *   cand_offsets [R + 1] CSR
+ *   w_req  [d_out, f_req^2]          w_cand [d_out, f_cand (f_req + f_cand)]
+ *   bias   [d_out] fp32 or NULL;     activation ROCS_ACT_NONE or ROCS_ACT_RELU
+ *   out    [N, d_out], not overlapping any input or the workspace
+ *   workspace  at least rocs_glm_fm_linear_workspace_size(R, N, f_req, f_cand,
+ *              emb_dim, d_out, dtype) bytes, 256-byte aligned; on return it
+ *              holds Y^R (bf16 or fp32 [R, f_req^2]) at offset 0, the rest is
+ *              scratch. For shapes without the fused kernel it also holds Y^C.
+ *
+ * Fused kernel: bf16, f_req = 32, f_cand = 8, emb_dim = 128, d_out a multiple
+ * of 64 up to 4096; it needs x_req, x_cand, w_req, w_cand, bias and out
+ * 16-byte aligned (ROCS_ERR_INVALID_ARGUMENT otherwise). Other shapes and
+ * fp32 run the interaction and linear kernels one after the other.
+ * ---------------------------------------------------------------------------
+ */
+size_t rocs_glm_fm_linear_workspace_size(int64_t num_requests, int64_t num_cand, int32_t f_req,
+                                         int32_t f_cand, int32_t emb_dim, int64_t d_out,
+                                         int32_t dtype);
+
+int32_t rocs_glm_fm_linear(const void* x_req, const void* x_cand, const int32_t* cand_offsets,
+                           int64_t num_requests, int64_t num_cand, int32_t f_req,
+                           int32_t f_cand, int32_t emb_dim, const void* w_req,
+                           const void* w_cand, const float* bias, int64_t d_out, int32_t dtype,
+                           int32_t activation, void* out, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * Index-map helpers (Section 4.1, m in {0..B_r-1}^{B_c}).
  *
  * rocs_request_ids: out_ids[n] = m_n for n < N, computed on the device by the

@@ -39,6 +39,9 @@ SIGNATURES = {
     "rocs_ikbo_mlp2_workspace_size": (_size, [_i64, _i64, _i64, _i64, _i64, _i64, _i32]),
     "rocs_ikbo_mlp2": (_i32, [_vp, _i64, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64,
                               _i64, _i64, _i32, _i32, _i32, _vp, _vp, _size, _vp]),
+    "rocs_glm_fm_linear_workspace_size": (_size, [_i64, _i64, _i32, _i32, _i32, _i64, _i32]),
+    "rocs_glm_fm_linear": (_i32, [_vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32, _vp, _vp, _vp,
+                                  _i64, _i32, _i32, _vp, _vp, _size, _vp]),
     "rocs_request_ids": (_i32, [_vp, _i64, _i64, _vp, _vp]),
     "rocs_validate_offsets": (_i32, [_vp, _i64, _i64, _vp]),
 }

@@ -14,7 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "librocs.so")
-SOURCES = ["api.hip", "linear.hip", "attention.hip", "interaction.hip", "lcb.hip", "mlp.hip"]
+SOURCES = ["api.hip", "linear.hip", "attention.hip", "interaction.hip", "lcb.hip", "mlp.hip",
+           "fmlinear.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

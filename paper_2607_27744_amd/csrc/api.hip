@@ -577,6 +577,106 @@ int32_t rocs_ikbo_mlp2(const void* x_req, int64_t k_req, const void* x_cand, int
   return ok();
 }
 
+static bool fm_linear_fused(int32_t f_req, int32_t f_cand, int32_t emb, int64_t d_out,
+                            int32_t dtype) {
+  return dtype == ROCS_DTYPE_BF16 && rocs::fm_linear_fused_shape(f_req, f_cand, emb, d_out);
+}
+
+size_t rocs_glm_fm_linear_workspace_size(int64_t num_requests, int64_t num_cand, int32_t f_req,
+                                         int32_t f_cand, int32_t emb_dim, int64_t d_out,
+                                         int32_t dtype) {
+  if (num_requests <= 0 || num_cand < 0 || f_req < 1 || f_cand < 1 || emb_dim < 1 ||
+      d_out < 1 || !valid_dtype(dtype))
+    return 0;
+  const size_t es = esize(dtype);
+  // Y^R [R, f_req^2], then Zb [R, d_out] fp32.
+  size_t n = align256((size_t)num_requests * f_req * f_req * es) +
+             align256((size_t)num_requests * (size_t)d_out * sizeof(float));
+  if (!fm_linear_fused(f_req, f_cand, emb_dim, d_out, dtype))   // Y^C and the index map
+    n += align256((size_t)num_cand * f_cand * (f_req + f_cand) * es) +
+         align256((size_t)num_cand * sizeof(int32_t));
+  return n;
+}
+
+int32_t rocs_glm_fm_linear(const void* x_req, const void* x_cand, const int32_t* cand_offsets,
+                           int64_t R, int64_t N, int32_t f_req, int32_t f_cand, int32_t emb,
+                           const void* w_req, const void* w_cand, const float* bias,
+                           int64_t d_out, int32_t dtype, int32_t activation, void* out,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
+  if (activation != ROCS_ACT_NONE && activation != ROCS_ACT_RELU)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown activation %d", activation);
+  if (R < 0 || N < 0 || f_req < 1 || f_cand < 1 || emb < 1 || d_out < 1)
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "need R >= 0, N >= 0, f_req >= 1, f_cand >= 1, emb_dim >= 1, d_out >= 1");
+  const int64_t k_req = (int64_t)f_req * f_req, k_cand = (int64_t)f_cand * (f_req + f_cand);
+  if (R > kMaxI32 || N * f_cand > kMaxI32 || N * k_cand > kMaxI32 || R * k_req > kMaxI32 ||
+      d_out > kMaxI32 || (int64_t)f_req * emb > (1 << 24) || (int64_t)f_cand * emb > (1 << 24))
+    return fail(ROCS_ERR_UNSUPPORTED, "size too large");
+  if (N == 0) return ok();
+  if (R == 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "N > 0 candidates but no requests");
+  if (x_req == nullptr || x_cand == nullptr || cand_offsets == nullptr || w_req == nullptr ||
+      w_cand == nullptr || out == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
+  const bool fused = fm_linear_fused(f_req, f_cand, emb, d_out, dtype);
+  if (fused && !(aligned(x_req, 16) && aligned(x_cand, 16) && aligned(w_req, 16) &&
+                 aligned(w_cand, 16) && aligned(bias, 16) && aligned(out, 16)))
+    return fail(ROCS_ERR_INVALID_ARGUMENT,
+                "the fused kernel needs 16-byte aligned x_req, x_cand, w_req, w_cand, bias "
+                "and out");
+  const size_t need = rocs_glm_fm_linear_workspace_size(R, N, f_req, f_cand, emb, d_out, dtype);
+  if (workspace == nullptr || workspace_bytes < need)
+    return fail(ROCS_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!aligned(workspace, 256))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  const size_t es = esize(dtype);
+  const size_t out_bytes = (size_t)N * d_out * es;
+  const struct { const void* p; size_t n; const char* name; } ins[] = {
+      {x_req, (size_t)R * f_req * emb * es, "x_req"},
+      {x_cand, (size_t)N * f_cand * emb * es, "x_cand"},
+      {cand_offsets, (size_t)(R + 1) * sizeof(int32_t), "cand_offsets"},
+      {w_req, (size_t)d_out * k_req * es, "w_req"},
+      {w_cand, (size_t)d_out * k_cand * es, "w_cand"},
+      {bias, (size_t)d_out * sizeof(float), "bias"},
+  };
+  for (const auto& in : ins) {
+    if (overlap(out, out_bytes, in.p, in.n))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "out overlaps %s", in.name);
+    if (overlap(workspace, need, in.p, in.n))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace overlaps %s", in.name);
+  }
+  if (overlap(workspace, need, out, out_bytes))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "workspace overlaps out");
+
+  rocs::FmLinearArgs a{};
+  a.x_req = x_req; a.x_cand = x_cand; a.cand_offsets = cand_offsets;
+  a.w_req = w_req; a.w_cand = w_cand; a.bias = bias;
+  a.R = R; a.N = N; a.d_out = d_out; a.f_req = f_req; a.f_cand = f_cand; a.emb = emb;
+  a.bf16 = dtype == ROCS_DTYPE_BF16;
+  a.relu = activation == ROCS_ACT_RELU;
+  a.out = out;
+  char* ws = static_cast<char*>(workspace);
+  a.y_req = ws;
+  size_t at = align256((size_t)R * k_req * es);
+  a.z = reinterpret_cast<float*>(ws + at);
+  at += align256((size_t)R * d_out * sizeof(float));
+  if (!fused) {
+    a.y_cand = ws + at;
+    at += align256((size_t)N * k_cand * es);
+    a.ids = reinterpret_cast<int32_t*>(ws + at);
+  }
+  a.interaction_fast = a.bf16 && f_req % 16 == 0 &&
+                       (f_cand == 4 || f_cand == 8 || f_cand == 16) && emb % 32 == 0 &&
+                       aligned(x_req, 16) && aligned(x_cand, 16);
+  a.linear_fast = a.bf16 && k_cand % 8 == 0 && k_req % 8 == 0 && d_out % 4 == 0 &&
+                  aligned(w_req, 16) && aligned(w_cand, 16) && aligned(bias, 16) &&
+                  aligned(out, 16);
+  const hipError_t e = rocs::launch_fm_linear(a, fused, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_glm_fm_linear: %s", hipGetErrorString(e));
+  return ok();
+}
+
 int32_t rocs_request_ids(const int32_t* cand_offsets, int64_t R, int64_t N, int32_t* out_ids,
                          void* stream) {
   if (R < 0 || N < 0) return fail(ROCS_ERR_INVALID_ARGUMENT, "negative size");

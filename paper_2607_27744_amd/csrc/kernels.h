@@ -88,6 +88,24 @@ struct Mlp2Args {
   void* h;              // [N, d_hidden] workspace of the two-launch form
 };
 
+struct FmLinearArgs {
+  const void* x_req;    // [R, f_req, emb]
+  const void* x_cand;   // [N, f_cand, emb]
+  const int32_t* cand_offsets;   // CSR [R + 1]
+  const void* w_req;    // [d_out, f_req^2]
+  const void* w_cand;   // [d_out, f_cand (f_req + f_cand)]
+  const float* bias;    // [d_out] or NULL
+  int64_t R, N, d_out;
+  int f_req, f_cand, emb;
+  bool bf16, relu;
+  bool interaction_fast, linear_fast;   // kernel choices of the two-operator form
+  void* out;            // [N, d_out]
+  void* y_req;          // [R, f_req^2] workspace (the request-side interaction)
+  void* y_cand;         // [N, f_cand (f_req + f_cand)] workspace (two-operator form only)
+  float* z;             // [R, d_out] workspace
+  int32_t* ids;         // [N] workspace (two-operator form only)
+};
+
 // Each returns hipSuccess or the launch error.
 hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t* ids,
                               hipStream_t s);
@@ -100,5 +118,7 @@ bool lcb_fast_shape(int f_cand, int o_cand, int emb);
 hipError_t launch_request_table(const LinearArgs& a, hipStream_t s);
 hipError_t launch_mlp2(const Mlp2Args& a, bool fused, hipStream_t s);
 bool mlp2_fused_shape(int64_t k_cand, int64_t d_hidden, int64_t d_out);
+hipError_t launch_fm_linear(const FmLinearArgs& a, bool fused, hipStream_t s);
+bool fm_linear_fused_shape(int f_req, int f_cand, int emb, int64_t d_out);
 
 }  // namespace rocs

@@ -16,7 +16,8 @@ from . import _lib
 __all__ = [
     "load_library", "ikbo_linear", "ikbo_linear_mapped", "glm_linear", "linear_workspace_size",
     "dca_attention", "dca_attention_mapped", "dca_request_attention", "glm_interaction",
-    "ikbo_lcb", "ikbo_lcb_mapped", "ikbo_mlp2", "mlp2_workspace_size", "request_ids",
+    "ikbo_lcb", "ikbo_lcb_mapped", "ikbo_mlp2", "mlp2_workspace_size", "glm_fm_linear",
+    "fm_linear_workspace_size", "request_ids",
     "validate_offsets", "RocsError",
 ]
 
@@ -234,6 +235,53 @@ def ikbo_mlp2(x_cand, w1_cand, w2, *, x_req=None, w1_req=None, cand_offsets=None
         _ptr(b2), _ptr(cand_offsets), n_req, n_cand, d_hidden, d_out, code, _ACT[activation1],
         _ACT[activation2], _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)),
         "rocs_ikbo_mlp2")
+    return out
+
+
+def fm_linear_workspace_size(num_requests, num_cand, f_req, f_cand, emb_dim, d_out, dtype):
+    code = _lib.DTYPE_BF16 if dtype == torch.bfloat16 else _lib.DTYPE_F32
+    return int(_lib.load().rocs_glm_fm_linear_workspace_size(num_requests, num_cand, f_req,
+                                                              f_cand, emb_dim, d_out, code))
+
+
+def glm_fm_linear(x_req, x_cand, cand_offsets, w_req, w_cand, *, bias=None, activation="relu",
+                  out=None, workspace=None, stream=None):
+    """rocs_glm_fm_linear: out[n] = act(w_req @ vec(Y^R[m_n]) + w_cand @ vec(Y^C[n]) + bias)
+    with Y^R, Y^C the GLM FM interaction of x_req [R, F_r, E] and x_cand [N, F_c, E].
+    w_req [D, F_r^2], w_cand [D, F_c (F_r + F_c)], bias [D] float32. Returns out [N, D];
+    the workspace then holds Y^R at its start."""
+    lib = _lib.load()
+    _need(x_req.dim() == 3 and x_cand.dim() == 3 and x_req.shape[2] == x_cand.shape[2],
+          "x_req [R, F_r, E] and x_cand [N, F_c, E] expected")
+    n_req, f_req, emb = x_req.shape
+    n_cand, f_cand = x_cand.shape[0], x_cand.shape[1]
+    _offsets(cand_offsets, n_req)
+    d_out = w_cand.shape[0]
+    _need(w_req.shape == (d_out, f_req * f_req), "w_req must be [d_out, f_req^2]")
+    _need(w_cand.shape == (d_out, f_cand * (f_req + f_cand)),
+          "w_cand must be [d_out, f_cand (f_req + f_cand)]")
+    code = _dtype_code(x_cand)
+    for t in (x_req, w_req, w_cand):
+        _need(t.dtype == x_cand.dtype, "inputs must share one dtype")
+    if bias is not None:
+        _need(bias.dtype == torch.float32 and bias.shape == (d_out,), "bias must be float32 [d_out]")
+    for t in (x_req, x_cand, w_req, w_cand, bias):
+        _need(t is None or t.is_contiguous(), "tensors must be contiguous")
+    if out is None:
+        out = torch.empty((n_cand, d_out), dtype=x_cand.dtype, device=x_cand.device)
+    _need(out.shape == (n_cand, d_out) and out.dtype == x_cand.dtype and out.is_contiguous(),
+          "out must be a contiguous [N, d_out] tensor of the input dtype")
+    need = int(lib.rocs_glm_fm_linear_workspace_size(n_req, n_cand, f_req, f_cand, emb, d_out,
+                                                     code))
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x_cand.device)
+    _on_gpu(x_req, x_cand, cand_offsets, w_req, w_cand, bias, out, workspace)
+    _need(activation in _ACT, f"activation must be one of {sorted(k for k in _ACT if k)}")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _lib.check(lib.rocs_glm_fm_linear(
+        _ptr(x_req), _ptr(x_cand), _ptr(cand_offsets), n_req, n_cand, f_req, f_cand, emb,
+        _ptr(w_req), _ptr(w_cand), _ptr(bias), d_out, code, _ACT[activation], _ptr(out),
+        _ptr(workspace), ws_bytes, _stream(stream)), "rocs_glm_fm_linear")
     return out
 
 

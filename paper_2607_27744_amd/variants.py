@@ -30,6 +30,9 @@ line with the call's algorithmic FLOPs and bytes against the MI355X peaks.
   mlp2              the retrieval MLP (64 requests, ~65k candidates, 1024+256
                     -> 512 ReLU -> 256) as one fused call with the hidden
                     layer on chip, timed beside the two linear launches
+  fm_linear         the interaction workload (128 requests x 512 candidates,
+                    32 + 8 fields of width 128, FM then 1024 + 320 -> 512
+                    ReLU) as one fused call, timed beside the two operators
 """
 
 import os
@@ -44,7 +47,7 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
 NAMES = ("lcb", "dca_tq32", "dca_tq64", "dca_request", "linear_mapped", "linear_combined",
-         "glm_linear", "dca_layer", "mlp2")
+         "glm_linear", "dca_layer", "mlp2", "fm_linear")
 
 
 def _bf16(a):
@@ -253,6 +256,34 @@ def _mlp2(steps, warmup):
                  ms, flops, byts, "mfma", n, "candidates", {"two_launch_ms": round(ms_two, 4)})
 
 
+def _fm_linear(steps, warmup):
+    w = wl.make_workload(4, seed=0)
+    n, r = w.n_cand, w.n_req
+    xr, xc, co = _bf16(w.x_req), _bf16(w.x_cand), _i32(w.cand_offsets)
+    wr, wc = _bf16(w.w_req), _bf16(w.w_cand)
+    out = torch.empty((n, 512), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(ops.fm_linear_workspace_size(r, n, 32, 8, 128, 512, torch.bfloat16),
+                     dtype=torch.uint8, device="cuda")
+    ms = _time(lambda: ops.glm_fm_linear(xr, xc, co, wr, wc, out=out, workspace=ws), steps,
+               warmup)
+    y_req = torch.empty((r, 1024), dtype=torch.bfloat16, device="cuda")
+    y_cand = torch.empty((n, 320), dtype=torch.bfloat16, device="cuda")
+    lws = torch.empty(ops.linear_workspace_size(r, n, 512, 1024), dtype=torch.uint8,
+                      device="cuda")
+
+    def two():
+        ops.glm_interaction(xr, xc, co, y_req=y_req, y_cand=y_cand)
+        ops.ikbo_linear(y_cand, wc, x_req=y_req, w_req=wr, cand_offsets=co, activation="relu",
+                        out=out, workspace=lws)
+    ms_two = _time(two, steps, warmup)
+    flops = (2.0 * n * (8 * 32 + 8 * 8) * 128 + 2.0 * n * 320 * 512
+             + 2.0 * r * 32 * 32 * 128 + 2.0 * r * 1024 * 512)
+    byts = 2.0 * (n * 8 * 128 + n * 512 + r * 32 * 128 + 1344 * 512)
+    return _line("fm_linear", {"requests": r, "candidates": n, "f_req": 32, "f_cand": 8,
+                               "emb": 128, "d_out": 512},
+                 ms, flops, byts, "hbm", n, "candidates", {"two_operator_ms": round(ms_two, 4)})
+
+
 def run(name, steps=20, warmup=3):
     """Time one variant; returns its JSON-ready record."""
     ops.load_library()
@@ -274,4 +305,6 @@ def run(name, steps=20, warmup=3):
         return _dca_layer(steps, warmup)
     if name == "mlp2":
         return _mlp2(steps, warmup)
+    if name == "fm_linear":
+        return _fm_linear(steps, warmup)
     raise ValueError(f"variant must be one of {NAMES}")

@@ -140,6 +140,26 @@ def fm_case(counts, f_req, f_cand, emb_dim, *, seed=0, config_id=300, bf16=True)
     )
 
 
+def fm_linear_case(counts, f_req, f_cand, emb_dim, d_out, *, seed=0, config_id=700,
+                   bf16=True, bias=True):
+    """An FM interaction feeding a linear: fm_case's embeddings plus [w_req |
+    w_cand] drawn as one [D, F_r^2 + F_c (F_r + F_c)] matrix with std
+    1/sqrt(fan_in) and a float32 bias with std 0.1 (None without bias).
+    Embeddings have std 1/sqrt(E) so interaction values stay O(1)."""
+    c = fm_case(counts, f_req, f_cand, emb_dim, seed=seed, config_id=config_id, bf16=bf16)
+    k_r, k_c = f_req * f_req, f_cand * (f_req + f_cand)
+    std = 1.0 / np.sqrt(emb_dim)
+    c.x_req = normal(tensor_rng(seed, config_id, 1), c.x_req.shape, std=std, bf16=bf16)
+    c.x_cand = normal(tensor_rng(seed, config_id, 2), c.x_cand.shape, std=std, bf16=bf16)
+    w = normal(tensor_rng(seed, config_id, 3), (d_out, k_r + k_c), std=1.0 / np.sqrt(k_r + k_c),
+               bf16=bf16)
+    c.w_req, c.w_cand = np.ascontiguousarray(w[:, :k_r]), np.ascontiguousarray(w[:, k_r:])
+    c.bias = (normal(tensor_rng(seed, config_id, 4), (d_out,), std=0.1, bf16=False)
+              if bias else None)
+    c.d_out = d_out
+    return c
+
+
 def lcb_case(counts, f_req, f_cand, o_req, o_cand, emb_dim, *, seed=0, config_id=400,
              bf16=True):
     """One two-group LCB problem: x_req [R, F_r, E], x_cand [N, F_c, E], w_rr

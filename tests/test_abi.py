@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 17
+    assert len(names) == 19
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -202,6 +202,33 @@ def test_mlp2_argument_errors(lib):
     assert call(ws_bytes=1 << 20, ws=P(0x80010)) == _lib.INVALID_ARGUMENT   # not 256-aligned
     assert call(ws_bytes=1 << 20, out=FAKE[1]) == _lib.INVALID_ARGUMENT     # out aliases x_cand
     assert call(ws_bytes=1 << 20, ws=FAKE[3]) == _lib.INVALID_ARGUMENT      # ws aliases w1_cand
+    assert call(N=0) == _lib.OK
+
+
+@no_gpu
+def test_fm_linear_argument_errors(lib):
+    # Every call below fails validation (or has nothing to do) before any launch.
+    def call(**kw):
+        a = dict(xr=FAKE[0], xc=FAKE[1], co=FAKE[2], R=2, N=16, fr=32, fc=8, e=128, wr=FAKE[3],
+                 wc=FAKE[4], bias=None, d=64, dtype=1, act=1, out=FAKE[5], ws=FAKE[6],
+                 ws_bytes=64, stream=None)
+        a.update(kw)
+        return lib.rocs_glm_fm_linear(*a.values())
+    size = lib.rocs_glm_fm_linear_workspace_size
+    assert size(2, 16, 32, 8, 128, 64, 1) == 4096 + 512            # Y^R + Zb (fused shape)
+    assert size(2, 16, 16, 4, 64, 64, 1) == 1024 + 512 + 2560 + 256  # + Y^C + index map
+    assert size(0, 16, 32, 8, 128, 64, 1) == 0
+    assert call(dtype=3) == _lib.INVALID_ARGUMENT
+    assert call(act=2) == _lib.INVALID_ARGUMENT
+    assert call(fc=0) == _lib.INVALID_ARGUMENT
+    assert call(co=None) == _lib.INVALID_ARGUMENT
+    assert call(wc=None) == _lib.INVALID_ARGUMENT
+    assert call(R=0) == _lib.INVALID_ARGUMENT
+    assert call(out=P(0x60008)) == _lib.INVALID_ARGUMENT           # fused kernel: misaligned
+    assert call() == _lib.WORKSPACE_TOO_SMALL
+    assert call(ws_bytes=1 << 20, ws=P(0x70010)) == _lib.INVALID_ARGUMENT   # not 256-aligned
+    assert call(ws_bytes=1 << 20, out=FAKE[4]) == _lib.INVALID_ARGUMENT     # out aliases w_cand
+    assert call(ws_bytes=1 << 20, ws=FAKE[0]) == _lib.INVALID_ARGUMENT      # ws aliases x_req
     assert call(N=0) == _lib.OK
 
 
