@@ -38,14 +38,15 @@ constexpr float kWeightBound = 0x1p64f;
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel (32x32x16 shape), head_dim D in {64, 128}.
 //
-// Workgroup: W waves x 32 query rows = one 32 W-row tile. With 32 rows a wave
-// needs under 256 VGPRs, so two waves share each SIMD and one wave's softmax
-// (VALU) overlaps the other's matrix-core work. head_dim 128 takes W = 8 (a
-// 256-row tile, one workgroup per CU: 128 KiB of K/V ring). head_dim 64 takes
-// W = 4: its 64 KiB ring lets two 128-row workgroups share a CU, so one
-// workgroup's prologue (query and first K/V loads), epilogue and request
-// lookup run while the other is in its main loop, and histories of a few
-// hundred rows (a ranking request) do not leave the CU waiting on memory.
+// Workgroup: 4 waves x 32 query rows = one 128-row tile. With 32 rows a wave
+// needs under 256 VGPRs, and each workgroup's K/V staging fits in 64 KiB of
+// LDS, so two workgroups share a CU: each SIMD runs one wave of each. The two
+// waves are not held in step by a common barrier, so one's softmax (VALU)
+// overlaps the other's matrix-core work, and one workgroup's prologue (request
+// lookup, query and first K/V loads) and epilogue run while the other is in
+// its main loop. (A 256-row workgroup of 8 waves, one per CU, reuses each K/V
+// stage for twice the rows but leaves those fixed costs exposed: 4% slower at
+// a history of 2048.)
 //
 // Scores are computed transposed, S^T = K Q^T (A = K rows from LDS, B = the
 // wave's query rows held in registers for the whole history), so each lane's
@@ -57,7 +58,7 @@ constexpr float kWeightBound = 0x1p64f;
 //
 // K/V staging: history rows go from HBM/L2 straight into LDS with the DMA
 // form of the global load (no VGPR round trip, no LDS store instructions),
-// two stages ahead of use through a 4-deep ring. Rows keep their HBM layout in
+// ahead of use through rings in LDS (see attn_slots). Rows keep their HBM layout in
 // LDS, with the 16-byte chunks of each row XOR-swizzled by the row index so
 // that both fragment reads are conflict-free; V^T fragments come out of the
 // row-major V stage through the transposing LDS read (ds_read_b64_tr_b16).
@@ -74,9 +75,12 @@ constexpr float kWeightBound = 0x1p64f;
 // and the keys past the history's end are masked (weight 0) in the last,
 // ragged stage only.
 // ---------------------------------------------------------------------------
-constexpr int kStages = 4;       // K/V ring depth in LDS (loads run two stages ahead)
-
-template <int D> constexpr int attn_waves() { return D == 64 ? 4 : 8; }
+template <int D> constexpr int attn_waves() { return 4; }  // query rows / 32 per workgroup
+// Slots per K (and V) ring: head_dim 64 keeps a 4-deep shared ring (K and V
+// of a stage loaded together, two stages ahead); head_dim 128 uses separate
+// 2-slot K and V rings (K one stage further ahead than V), 64 KiB in all, so
+// two workgroups share a CU.
+template <int D> constexpr int attn_slots() { return D == 64 ? 4 : 2; }
 
 template <int D, int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void dca_attn_bf16(
@@ -98,6 +102,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   constexpr int NL = 2 * NI;                          // DMA loads per thread per stage
   static_assert(NI >= 1 && kTileKeys % (KPI * W) == 0, "staging does not tile");
   static_assert(CR * 16 == ROWB, "layout");
+  constexpr int kStages = attn_slots<D>();
   static_assert(kStages * STAGE <= 65536, "LDS offsets must fit the 16-bit immediate");
   __shared__ __attribute__((aligned(1024))) char lds[2 * kStages * STAGE];  // K ring, V ring
   ROCS_LDS char* const lds3 = (ROCS_LDS char*)lds;
@@ -153,26 +158,26 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
     soff[i] = (uint32_t)(skey[i] * rowstride) + schunk[i];
   }
   const uint32_t lds_base = lds_addr(lds);
-  auto issue = [&](int t) {
+  // Stage t of one operand (K: ring 0, V: ring 1) into slot t % kStages.
+  auto issue_op = [&](int t, int ring) {
     const int base = t * kTileKeys;
-    const uint32_t kdst = lds_base + (uint32_t)((t % kStages) * STAGE);
-    const uint32_t vdst = kdst + kStages * STAGE;
+    const char* src = ring == 0 ? kbase : vbase;
+    const uint32_t dst = lds_base + (uint32_t)((ring * kStages + t % kStages) * STAGE);
     if (base + kTileKeys <= L) {
-      const char* ks = kbase + base * rowstride;
-      const char* vs = vbase + base * rowstride;
+      const char* ss = src + base * rowstride;
 #pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        lds_dma16_sv(ks, soff[i], kdst + KPI * (NI * wave + i) * ROWB);
-        lds_dma16_sv(vs, soff[i], vdst + KPI * (NI * wave + i) * ROWB);
-      }
+      for (int i = 0; i < NI; ++i) lds_dma16_sv(ss, soff[i], dst + KPI * (NI * wave + i) * ROWB);
     } else {
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int64_t o = (int64_t)min(base + skey[i], L - 1) * rowstride + schunk[i];
-        lds_dma16(kbase + o, kdst + KPI * (NI * wave + i) * ROWB);
-        lds_dma16(vbase + o, vdst + KPI * (NI * wave + i) * ROWB);
+        lds_dma16(src + o, dst + KPI * (NI * wave + i) * ROWB);
       }
     }
+  };
+  auto issue = [&](int t) {
+    issue_op(t, 0);
+    issue_op(t, 1);
   };
 
   // LDS fragment addresses (bytes, stage 0). K: row 32 kb + l32, chunk
@@ -336,11 +341,17 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
 
   // Software pipeline over stages: while the matrix cores compute the scores
   // of stage t + 1, the VALU runs the softmax of stage t, then stage t's PV
-  // product follows. Stage t + 3 is being loaded meanwhile; one barrier per
-  // stage hands the ring slots around.
-  issue(0);
-  if (ntiles > 1) issue(1);
-  if (ntiles > 2) issue(2);
+  // product follows. Meanwhile stage t + 3 is loaded (4-slot ring), or K of
+  // stage t + 2 and V of stage t + 1 (2-slot rings); one barrier per stage
+  // hands the ring slots around.
+  if constexpr (kStages == 4) {
+    issue(0);
+    if (ntiles > 1) issue(1);
+    if (ntiles > 2) issue(2);
+  } else {
+    issue(0);
+    if (ntiles > 1) issue_op(1, 0);
+  }
   // Everything resident, the query fragments included: from here on the
   // only vector-memory operations in flight are the ring's DMA loads, which
   // the compiler does not track, so it adds no waits of its own in the loop.
@@ -348,15 +359,24 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   ring_barrier();
   f32x16 s_a[KB], s_b[KB];
   auto step = [&](int kt, f32x16 (&s_cur)[KB], f32x16 (&s_next)[KB]) {
-    const bool fill = kt + 3 < ntiles;
-    if (fill) issue(kt + 3);
-    if (active) {
-      stage((kt + 1) % kStages, s_next, kt % kStages, s_cur);
+    if constexpr (kStages == 4) {
+      const bool fill = kt + 3 < ntiles;
+      if (fill) issue(kt + 3);
+      if (active) stage((kt + 1) % kStages, s_next, kt % kStages, s_cur);
+      if (fill) wait_vmcnt<NL>(); else wait_vmcnt<0>();   // stage kt + 2 resident
+    } else {
+      // This step reads K of stage kt + 1 and V of stage kt; their other
+      // slots (K of kt, V of kt - 1) were released by the last barrier.
+      if (kt + 2 < ntiles) issue_op(kt + 2, 0);
+      if (kt + 1 < ntiles) issue_op(kt + 1, 1);
+      if (active) stage((kt + 1) % kStages, s_next, kt % kStages, s_cur);
+      wait_vmcnt<0>();                                      // K of kt + 2, V of kt + 1
     }
-    if (fill) wait_vmcnt<NL>(); else wait_vmcnt<0>();     // stage kt + 2 resident
     ring_barrier();
   };
   if (active) qk(0, s_a);
+  // Two-slot rings: step 0 reloads K slot 0, which qk(0) has just read.
+  if constexpr (kStages == 2) ring_barrier();
   int kt = 0;
   for (; kt + 2 < ntiles; kt += 2) {        // unrolled by two: the score buffers swap roles
     step(kt, s_a, s_b);
