@@ -13,11 +13,12 @@ from paper_2607_27744_amd import workloads as wl
 pytestmark = pytest.mark.gpu
 
 # (candidate counts, history lengths): empty requests, empty histories,
-# histories of 1 and around the 64-key stage, candidate counts around the
-# 256-row tile.
+# histories of 1, around the 64-key stage and of two and three stages,
+# candidate counts around the 128-row tile and its multiples.
 SHAPES = [
     ([300, 1, 0, 211], [70, 5, 0, 129]),
     ([256, 257, 255], [64, 65, 63]),
+    ([127, 128, 129], [128, 130, 191]),
     ([1], [1]),
     ([40, 500], [1000, 300]),
 ]
