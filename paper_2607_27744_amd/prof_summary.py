@@ -5,6 +5,7 @@
     python -m paper_2607_27744_amd.prof_summary traffic <fetch_dir> <write_dir> \
         <copy_fetch_dir> <copy_write_dir> <kernel-substring> <name>
     python -m paper_2607_27744_amd.prof_summary copy     (run under rocprofv3 --pmc)
+    python -m paper_2607_27744_amd.prof_summary sq <kernel-substring> <name> <pmc_dir>...
 
 `stats` prints the per-kernel duration table (ms) of a --kernel-trace --stats
 run. `copy` performs three plain 1 GiB device-to-device copies (the calibration
@@ -12,7 +13,11 @@ workload for the counters). `traffic` averages FETCH_SIZE and WRITE_SIZE (KiB pe
 kernels whose name contains the substring, scales each by what the same
 counter reads for a plain device copy of known size (the calibration runs),
 and prints a JSON record with the source hash of the kernel's files, which
-bench.py compares before it reports the figure.
+bench.py compares before it reports the figure. `sq` reads shader-sequencer
+(SQ_*) counter passes of the matching kernels and prints where the time goes:
+the shader clock the kernel ran at (CU-busy cycles per CU over the dispatch
+duration), the share of SIMD cycles the matrix cores were busy, and how the
+waves' cycles split between issuing and waiting.
 """
 
 import csv
@@ -101,6 +106,43 @@ def traffic(fetch_dir, write_dir, copy_fetch, copy_write, substring, name):
     print(json.dumps(rec, indent=1))
 
 
+def sq(substring, name, *dirs):
+    vals, durs, cus, simds = {}, [], 256, 4
+    for d in dirs:
+        for r in _rows(d):
+            if substring not in r["Kernel_Name"]:
+                continue
+            vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            if r["Counter_Name"] == "SQ_BUSY_CU_CYCLES":
+                durs.append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        for r in _rows(d, "*agent_info.csv"):
+            if r.get("Agent_Type") == "GPU":
+                cus, simds = int(r["Cu_Count"]), int(r["Simd_Per_Cu"])
+    if not vals:
+        raise SystemExit(f"no SQ rows for kernels matching {substring!r}")
+    m = {k: sum(v) / len(v) for k, v in vals.items()}
+    rec = {"name": name, "kernel": substring, "dispatches": len(durs),
+           "counters": {k: round(v) for k, v in sorted(m.items())}}
+    key = next((k for k in KERNEL_SOURCES if k in substring), None)
+    if key is not None:
+        rec["source_sha256"] = source_hash(key)
+    if durs and "SQ_BUSY_CU_CYCLES" in m:
+        dur_ns = sum(durs) / len(durs)
+        cu_cycles = m["SQ_BUSY_CU_CYCLES"] / cus
+        rec["duration_ms"] = round(dur_ns / 1e6, 4)
+        rec["clock_ghz"] = round(cu_cycles / dur_ns, 3)
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in m:
+            rec["mfma_busy"] = round(m["SQ_VALU_MFMA_BUSY_CYCLES"] / (m["SQ_BUSY_CU_CYCLES"] * simds), 4)
+    # Wave-state counters count in units of four cycles, as SQ_WAVE_CYCLES does.
+    if "SQ_WAVE_CYCLES" in m:
+        rec["wave_cycle_shares"] = {
+            k[3:].lower(): round(m[k] / m["SQ_WAVE_CYCLES"], 4)
+            for k in ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_ANY",
+                      "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_SCA",
+                      "SQ_ACTIVE_INST_MISC") if k in m}
+    print(json.dumps(rec, indent=1))
+
+
 def copy():
     """Three 1 GiB bf16 device copies (hipMemcpyAsync's copy kernel)."""
     import torch
@@ -122,5 +164,7 @@ if __name__ == "__main__":
         trace(sys.argv[2])
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:8])
+    elif sys.argv[1] == "sq":
+        sq(*sys.argv[2:])
     else:
         raise SystemExit(__doc__)
