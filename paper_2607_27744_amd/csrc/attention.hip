@@ -58,7 +58,9 @@ constexpr float kWeightBound = 0x1p64f;
 //
 // K/V staging: history rows go from HBM/L2 straight into LDS with the DMA
 // form of the global load (no VGPR round trip, no LDS store instructions),
-// ahead of use through rings in LDS (see attn_slots). Rows keep their HBM layout in
+// ahead of use through two 2-slot rings in LDS, one for K and one for V (K of
+// stage t + 2 and V of stage t + 1 load while stage t is processed). Rows keep
+// their HBM layout in
 // LDS, with the 16-byte chunks of each row XOR-swizzled by the row index so
 // that both fragment reads are conflict-free; V^T fragments come out of the
 // row-major V stage through the transposing LDS read (ds_read_b64_tr_b16).
@@ -76,11 +78,11 @@ constexpr float kWeightBound = 0x1p64f;
 // ragged stage only.
 // ---------------------------------------------------------------------------
 template <int D> constexpr int attn_waves() { return 4; }  // query rows / 32 per workgroup
-// Slots per K (and V) ring: head_dim 64 keeps a 4-deep shared ring (K and V
-// of a stage loaded together, two stages ahead); head_dim 128 uses separate
-// 2-slot K and V rings (K one stage further ahead than V), 64 KiB in all, so
-// two workgroups share a CU.
-template <int D> constexpr int attn_slots() { return D == 64 ? 4 : 2; }
+// Slots per K (and per V) ring: 4 stages in LDS, 64 KiB at head_dim 128, so
+// two workgroups share a CU. (At head_dim 64 a single 4-slot ring holding K
+// and V of a stage together, loaded three stages ahead, measured 5% slower
+// on ranking-sized histories.)
+constexpr int kRingSlots = 2;
 
 template <int D, int W>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void dca_attn_bf16(
@@ -99,10 +101,9 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   constexpr int STAGE = kTileKeys * ROWB;             // bytes of one K (or V) stage
   constexpr int KPI = 1024 / ROWB;                    // rows per wave-wide DMA load
   constexpr int NI = kTileKeys / (KPI * W);           // DMA loads per wave, operand, stage
-  constexpr int NL = 2 * NI;                          // DMA loads per thread per stage
   static_assert(NI >= 1 && kTileKeys % (KPI * W) == 0, "staging does not tile");
   static_assert(CR * 16 == ROWB, "layout");
-  constexpr int kStages = attn_slots<D>();
+  constexpr int kStages = kRingSlots;
   static_assert(kStages * STAGE <= 65536, "LDS offsets must fit the 16-bit immediate");
   __shared__ __attribute__((aligned(1024))) char lds[2 * kStages * STAGE];  // K ring, V ring
   ROCS_LDS char* const lds3 = (ROCS_LDS char*)lds;
@@ -348,17 +349,10 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
 
   // Software pipeline over stages: while the matrix cores compute the scores
   // of stage t + 1, the VALU runs the softmax of stage t, then stage t's PV
-  // product follows. Meanwhile stage t + 3 is loaded (4-slot ring), or K of
-  // stage t + 2 and V of stage t + 1 (2-slot rings); one barrier per stage
-  // hands the ring slots around.
-  if constexpr (kStages == 4) {
-    issue(0);
-    if (ntiles > 1) issue(1);
-    if (ntiles > 2) issue(2);
-  } else {
-    issue(0);
-    if (ntiles > 1) issue_op(1, 0);
-  }
+  // product follows. Meanwhile K of stage t + 2 and V of stage t + 1 are
+  // loaded; one barrier per stage hands the ring slots around.
+  issue(0);
+  if (ntiles > 1) issue_op(1, 0);
   // Everything resident, the query fragments included: from here on the
   // only vector-memory operations in flight are the ring's DMA loads, which
   // the compiler does not track, so it adds no waits of its own in the loop.
@@ -366,24 +360,17 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   ring_barrier();
   f32x16 s_a[KB], s_b[KB];
   auto step = [&](int kt, f32x16 (&s_cur)[KB], f32x16 (&s_next)[KB]) {
-    if constexpr (kStages == 4) {
-      const bool fill = kt + 3 < ntiles;
-      if (fill) issue(kt + 3);
-      if (active) stage((kt + 1) % kStages, s_next, kt % kStages, s_cur);
-      if (fill) wait_vmcnt<NL>(); else wait_vmcnt<0>();   // stage kt + 2 resident
-    } else {
-      // This step reads K of stage kt + 1 and V of stage kt; their other
-      // slots (K of kt, V of kt - 1) were released by the last barrier.
-      if (kt + 2 < ntiles) issue_op(kt + 2, 0);
-      if (kt + 1 < ntiles) issue_op(kt + 1, 1);
-      if (active) stage((kt + 1) % kStages, s_next, kt % kStages, s_cur);
-      wait_vmcnt<0>();                                      // K of kt + 2, V of kt + 1
-    }
+    // This step reads K of stage kt + 1 and V of stage kt; their other slots
+    // (K of kt, V of kt - 1) were released by the last barrier.
+    if (kt + 2 < ntiles) issue_op(kt + 2, 0);
+    if (kt + 1 < ntiles) issue_op(kt + 1, 1);
+    if (active) stage((kt + 1) % kStages, s_next, kt % kStages, s_cur);
+    wait_vmcnt<0>();                                        // K of kt + 2, V of kt + 1
     ring_barrier();
   };
   if (active) qk(0, s_a);
-  // Two-slot rings: step 0 reloads K slot 0, which qk(0) has just read.
-  if constexpr (kStages == 2) ring_barrier();
+  // Step 0 reloads K slot 0, which qk(0) has just read.
+  ring_barrier();
   int kt = 0;
   for (; kt + 2 < ntiles; kt += 2) {        // unrolled by two: the score buffers swap roles
     step(kt, s_a, s_b);
