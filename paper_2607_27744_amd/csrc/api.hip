@@ -462,10 +462,10 @@ int32_t rocs_ikbo_lcb_mapped(const void* x_req, const void* x_cand, const void* 
 
 // The fused two-layer kernel's shapes (bf16). Other shapes and fp32 run the
 // two-launch form, which keeps H in the workspace.
-static bool mlp2_fused(int64_t k_req, int64_t k_cand, int64_t d_hidden, int64_t d_out,
-                       int32_t dtype) {
+static bool mlp2_fused(int64_t R, int64_t k_req, int64_t k_cand, int64_t d_hidden,
+                       int64_t d_out, int32_t dtype) {
   return dtype == ROCS_DTYPE_BF16 && k_req % 8 == 0 &&
-         rocs::mlp2_fused_shape(k_cand, d_hidden, d_out);
+         rocs::mlp2_fused_shape(R, k_cand, d_hidden, d_out);
 }
 
 size_t rocs_ikbo_mlp2_workspace_size(int64_t num_requests, int64_t num_cand, int64_t k_req,
@@ -478,7 +478,7 @@ size_t rocs_ikbo_mlp2_workspace_size(int64_t num_requests, int64_t num_cand, int
   const bool req = k_req > 0 && num_requests > 0;
   // Request table Zb [R, d_hidden] fp32.
   if (req) n += align256((size_t)num_requests * (size_t)d_hidden * sizeof(float));
-  if (!mlp2_fused(k_req, k_cand, d_hidden, d_out, dtype)) {
+  if (!mlp2_fused(num_requests, k_req, k_cand, d_hidden, d_out, dtype)) {
     if (req) n += align256((size_t)num_cand * sizeof(int32_t));   // index map
     n += align256((size_t)num_cand * (size_t)d_hidden * esize(dtype));   // H
   }
@@ -509,7 +509,7 @@ int32_t rocs_ikbo_mlp2(const void* x_req, int64_t k_req, const void* x_cand, int
     return fail(ROCS_ERR_INVALID_ARGUMENT, "x_cand, w1_cand, w2 and out must not be NULL");
   if (k_req > 0 && (x_req == nullptr || w1_req == nullptr || cand_offsets == nullptr))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "k_req > 0 needs x_req, w1_req and cand_offsets");
-  const bool fused = mlp2_fused(k_req, k_cand, d_hidden, d_out, dtype);
+  const bool fused = mlp2_fused(R, k_req, k_cand, d_hidden, d_out, dtype);
   if (fused && !(aligned(x_cand, 16) && aligned(w1_cand, 16) && aligned(w2, 16) &&
                  aligned(out, 16) && aligned(b1, 16) && aligned(b2, 16) &&
                  aligned(x_req, 16) && aligned(w1_req, 16)))

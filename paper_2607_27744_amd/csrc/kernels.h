@@ -117,7 +117,7 @@ bool lcb_fast_shape(int f_cand, int o_cand, int emb);
 // The request table Zb = x_req W_req^T + bias (fp32, [R, d_out]) alone, bf16 in.
 hipError_t launch_request_table(const LinearArgs& a, hipStream_t s);
 hipError_t launch_mlp2(const Mlp2Args& a, bool fused, hipStream_t s);
-bool mlp2_fused_shape(int64_t k_cand, int64_t d_hidden, int64_t d_out);
+bool mlp2_fused_shape(int64_t R, int64_t k_cand, int64_t d_hidden, int64_t d_out);
 hipError_t launch_fm_linear(const FmLinearArgs& a, bool fused, hipStream_t s);
 bool fm_linear_fused_shape(int f_req, int f_cand, int emb, int64_t d_out);
 

@@ -858,8 +858,10 @@ hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
   }
   // The streaming kernel needs request-aligned tiles, i.e. CSR offsets; a
   // caller's per-candidate map takes the kernel with per-row request lookup.
+  // (K and D bounds: the kernel's per-lane load and store offsets within a
+  // 256-row tile are 32-bit.)
   const bool stream = !a.ids_given && a.x_cand_add == nullptr && a.k_cand % kStreamBK == 0 &&
-                      a.k_cand < (int64_t(1) << 22) &&
+                      a.k_cand < (int64_t(1) << 22) && a.d_out < (int64_t(1) << 22) &&
                       ((a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN) *
                               ((a.d_out + kStreamBM - 1) / kStreamBM) < (int64_t(1) << 31);
   // On request, the streaming kernel also runs the request side (combined

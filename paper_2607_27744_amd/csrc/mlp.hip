@@ -368,9 +368,12 @@ hipError_t launch_fused(const Mlp2Args& a, const float* zb, int64_t zb_stride,
 
 }  // namespace
 
-bool mlp2_fused_shape(int64_t k_cand, int64_t d_hidden, int64_t d_out) {
+bool mlp2_fused_shape(int64_t R, int64_t k_cand, int64_t d_hidden, int64_t d_out) {
+  // The second Zb row of a tile is addressed by a 32-bit byte offset from
+  // the first: the request table must stay under 4 GiB.
   return (k_cand == 128 || k_cand == 256) && (d_out == 128 || d_out == 256) &&
-         d_hidden >= kMlpHC && d_hidden % kMlpHC == 0 && d_hidden <= kMlpMaxHidden;
+         d_hidden >= kMlpHC && d_hidden % kMlpHC == 0 && d_hidden <= kMlpMaxHidden &&
+         R * d_hidden * 4 < (int64_t(1) << 32);
 }
 
 hipError_t launch_mlp2(const Mlp2Args& a, bool fused, hipStream_t s) {

@@ -188,6 +188,11 @@ def test_mlp2_argument_errors(lib):
     assert size(2, 16, 0, 128, 64, 128, 1) == 0                    # fused, no request term
     assert size(2, 16, 8, 128, 64, 128, 0) == 512 + 256 + 4096     # fp32: two launches
     assert size(2, 0, 8, 128, 64, 128, 1) == 0
+    # A request table of 4 GiB or more (R * d_hidden * 4 bytes) leaves the
+    # fused kernel's 32-bit Zb offsets: the two-launch form (with H) is sized.
+    big = (1 << 32) // (4 * 1024)
+    assert size(big - 1, 16, 8, 128, 1024, 128, 1) == (big - 1) * 4096
+    assert size(big, 16, 8, 128, 1024, 128, 1) == big * 4096 + 256 + 16 * 1024 * 2
     assert call(dtype=7) == _lib.INVALID_ARGUMENT
     assert call(a1=3) == _lib.INVALID_ARGUMENT
     assert call(a2=-1) == _lib.INVALID_ARGUMENT
