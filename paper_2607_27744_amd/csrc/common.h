@@ -159,6 +159,11 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// LDS byte address of a __shared__ object (wave-uniform).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const ROCS_LDS void*)p);
+}
+
 // 16 bytes per lane from global memory straight into LDS (the DMA form of
 // global_load_dwordx4): lane i's bytes land at dst + 16 i, dst wave-uniform.
 // Written as inline assembly on purpose: the compiler does not see an LDS
@@ -166,12 +171,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 // alias check would otherwise wait for every DMA load in flight before each
 // LDS read of the ring). The caller orders LDS reads after the loads with
 // wait_vmcnt and a barrier. The compiler does not count these loads either,
-// which only makes its own vector-memory waits stricter.
-// LDS byte address of a __shared__ object (wave-uniform).
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const ROCS_LDS void*)p);
-}
-// `dst` is an LDS byte address, wave-uniform.
+// which only makes its own vector-memory waits stricter. `dst` is an LDS
+// byte address, wave-uniform.
 __device__ __forceinline__ void lds_dma16(const void* src, uint32_t dst) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" :: "v"(src), "s"(dst) : "m0");
 }

@@ -69,15 +69,19 @@ __device__ __forceinline__ bool request_tile(
   const bool dok = d0 + row < D, rok = r0 + row < R;
   const bf16_t* wp = w + (int64_t)(d0 + row) * K + kq;
   const bf16_t* xp = x + (int64_t)(r0 + row) * K + kq;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  // Four waves split K; in a larger workgroup (the streaming kernel's) the
+  // other waves only join the barriers, so both launch forms sum alike.
+  if (wave < 4) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
-  for (int k = wave * 32; k < K; k += 128) {
-    const bool kok = k + kq < K;
-    const bf16x8 a = as_bf16x8(load16(wp + k, dok && kok));
-    const bf16x8 b = as_bf16x8(load16(xp + k, rok && kok));
-    acc = mfma16(a, b, acc);   // acc[i] = Z[r0 + row][d0 + 4 (lane / 16) + i]
+    for (int k = wave * 32; k < K; k += 128) {
+      const bool kok = k + kq < K;
+      const bf16x8 a = as_bf16x8(load16(wp + k, dok && kok));
+      const bf16x8 b = as_bf16x8(load16(xp + k, rok && kok));
+      acc = mfma16(a, b, acc);   // acc[i] = Z[r0 + row][d0 + 4 (lane / 16) + i]
+    }
+    red[wave * kWave + lane] = acc;
   }
-  red[wave * kWave + lane] = acc;
   __syncthreads();
   if (wave == 0) {
     f32x4 s = ((red[lane] + red[kWave + lane]) + red[2 * kWave + lane]) + red[3 * kWave + lane];
@@ -273,9 +277,10 @@ void ikbo_gemm_bf16(
 // Streaming candidate GEMM (bf16, K a multiple of 64), the main path.
 //
 // Persistent workgroups, one per CU, walk the 256 (features) x 256
-// (candidates) output tiles with a stride of the grid; four waves, one per
-// SIMD, each own a 128 x 128 quarter (16 MFMA 32x32 accumulators, 256 of the
-// wave's 512 registers). K arrives in 64-wide slabs (128-byte row segments:
+// (candidates) output tiles with a stride of the grid; eight waves, two per
+// SIMD, each own a 64 x 128 block (8 MFMA 32x32 accumulators, 128 of the
+// wave's 256 registers), so one wave's stalls (slab waits, fragment reads,
+// the epilogue's stores) leave the SIMD to the other. K arrives in 64-wide slabs (128-byte row segments:
 // whole cache lines, which the L2 serves at twice the rate of half lines)
 // through LDS rings filled by LDS DMA loads, as one stream across tile
 // boundaries: the weight slab (L2-resident) one slab ahead of use in a
@@ -397,7 +402,7 @@ uint64_t next_epoch() {
 }
 
 template <bool HAS_ZB, bool RELU, bool FUSED>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w,
                       const float* __restrict__ zb, const int32_t* __restrict__ off_g,
                       bf16_t* __restrict__ out, int R, int64_t N, int K, int D, int tiles_m,
@@ -406,10 +411,10 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   constexpr int NSA = 2, NSB = 3;                // ring depths: weights, candidates
   constexpr int ROWB = BK * 2;                   // bytes of one slab row (128)
   constexpr int RPI = 1024 / ROWB;               // slab rows per wave-wide DMA load (8)
-  constexpr int NI = BM / RPI / 4;               // DMA loads per wave and operand (8)
+  constexpr int NI = BM / RPI / 8;               // DMA loads per wave and operand (4)
   constexpr int SLAB = BM * ROWB;                // bytes of one operand slab (32 KiB)
   constexpr int BBASE = NSA * SLAB;              // candidate ring after the weight ring
-  static_assert(BM == BN && NI * RPI * 4 == BM && ROWB == 128, "tiling");
+  static_assert(BM == BN && NI * RPI * 8 == BM && ROWB == 128, "tiling");
   static_assert((NSA + NSB) * SLAB <= 160 * 1024, "LDS");
   __shared__ __attribute__((aligned(1024))) char lds[(NSA + NSB) * SLAB];
   ROCS_LDS char* const lds3 = (ROCS_LDS char*)lds;
@@ -421,7 +426,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5, h4 = 4 * hh;
-  const int wm0 = (wave & 1) * 128, wn0 = (wave >> 1) * 128;
+  const int wm0 = (wave & 3) * 64, wn0 = (wave >> 2) * 128;
   const int nk = K / BK;
   const int rowb = K * 2;
   const int logical = (int)xcd_remap(blockIdx.x, gridDim.x);
@@ -501,7 +506,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     buf_a ^= 1;
     a_queued = false;
   };
-  // Piece p of the planned loads: weights 0..7, candidates 8..15.
+  // Piece p of the planned loads: weights 0..NI-1, candidates NI..2NI-1.
   auto dma_plan_piece = [&](int p) __attribute__((always_inline)) {
     if (p < NI) {
       if (pa_on) dma_piece(pa_src, pa_lim, pa_dst, p);
@@ -513,18 +518,18 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   // Fragment addresses within an operand slab: row 32 f + l32 of the wave's
   // quarter, chunk 2 ks + hh; the swizzle turns the ks step into XOR 32 ks.
   const uint32_t fa0 = (uint32_t)(l32 * ROWB + 16 * (hh ^ ((l32 >> 1) & 7)));
-  f32x16 acc[4][4];
+  f32x16 acc[2][4];
   int cbuf_a = 0, cbuf_b = 0;            // ring slots of the slab being computed
   auto compute = [&](auto first_slab) __attribute__((always_inline)) {
     const uint32_t sa = (uint32_t)(cbuf_a * SLAB) + wm0 * ROWB;
     const uint32_t sb = (uint32_t)(BBASE + cbuf_b * SLAB) + wn0 * ROWB;
     // Fragments double-buffered across k-steps: the reads of step ks + 1 are
     // in flight while the MFMAs of step ks run.
-    bf16x8 af[2][4], bfr[2][4];
+    bf16x8 af[2][2], bfr[2][4];
     auto load_frags = [&](int ks, int slot) __attribute__((always_inline)) {
 #pragma unroll
       for (int f = 0; f < 4; ++f) {
-        af[slot][f] = *reinterpret_cast<const ROCS_LDS bf16x8*>(lds3 + sa + 32 * f * ROWB + (fa0 ^ (32u * ks)));
+        if (f < 2) af[slot][f] = *reinterpret_cast<const ROCS_LDS bf16x8*>(lds3 + sa + 32 * f * ROWB + (fa0 ^ (32u * ks)));
         bfr[slot][f] = *reinterpret_cast<const ROCS_LDS bf16x8*>(lds3 + sb + 32 * f * ROWB + (fa0 ^ (32u * ks)));
       }
     };
@@ -535,7 +540,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
       if (ks + 1 < BK / 16) load_frags(ks + 1, cur ^ 1);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int fm = 0; fm < 4; ++fm) {
+      for (int fm = 0; fm < 2; ++fm) {
 #pragma unroll
         for (int fn = 0; fn < 4; ++fn) {
           if constexpr (decltype(first_slab)::value) {
@@ -547,7 +552,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
           }
           acc[fm][fn] = mfma32(af[cur][fm], bfr[cur][fn], acc[fm][fn]);
         }
-        dma_plan_piece(4 * ks + fm);
+        dma_plan_piece(2 * ks + fm);
         // Keep MFMAs and loads in this order; ALU work may move.
         __builtin_amdgcn_sched_barrier(0x0002 | 0x0004);
       }
@@ -558,13 +563,13 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   // after the tile's last MFMAs (the fragment registers are free then) and
   // added in the epilogue. The buffer's extent is the request's row, so
   // features past D read as zero.
-  f32x4 zv[4][4];
+  f32x4 zv[2][4];
   auto load_zb = [&](const StreamTile& c) __attribute__((always_inline)) {
     if constexpr (HAS_ZB) {
       const auto rz = buffer_rsrc(zb + (int64_t)c.r * D, (uint32_t)D * 4u);
       const uint32_t vo = 4u * (uint32_t)(c.m0 + wm0 + h4);
 #pragma unroll
-      for (int fm = 0; fm < 4; ++fm)
+      for (int fm = 0; fm < 2; ++fm)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
           zv[fm][q] = __builtin_bit_cast(
@@ -608,7 +613,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   };
 
   // Epilogue. Element 4 q + i of acc[fm][fn] is feature 32 fm + 8 q + h4 + i
-  // of candidate 32 fn + l32 (within the wave's quarter). For q = 2j, 2j + 1
+  // of candidate 32 fn + l32 (within the wave's block). For q = 2j, 2j + 1
   // the lower half-wave keeps its q = 2j words and takes the upper half's,
   // the upper half keeps q = 2j + 1 and takes the lower half's: then lane
   // (l32, hh) holds features 32 fm + 16 j + 8 hh .. +7, one 16-byte store.
@@ -650,7 +655,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
       for (int fn = 0; fn < 4; ++fn) {
         const uint32_t vr = vo + 64u * (uint32_t)fn * (uint32_t)D;
 #pragma unroll
-        for (int fm = 0; fm < 4; ++fm)
+        for (int fm = 0; fm < 2; ++fm)
 #pragma unroll
           for (int j = 0; j < 2; ++j)
             __builtin_amdgcn_raw_buffer_store_b128(swapped(fm, fn, j), ro, vr + 2u * (32 * fm + 16 * j), 0, 0);
@@ -661,7 +666,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     for (int fn = 0; fn < 4; ++fn) {
       const int rr = wn0 + 32 * fn + l32;
 #pragma unroll
-      for (int fm = 0; fm < 4; ++fm)
+      for (int fm = 0; fm < 2; ++fm)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           // The swap is wave-wide: every lane takes part, only valid ones
@@ -914,7 +919,7 @@ hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
       fr.n_tiles = req_tiles;
     }
     auto go = [&](auto kernel) {
-      return launch_kernel(kernel, dim3((uint32_t)grid), dim3(256), s, x, w, zb, off, o,
+      return launch_kernel(kernel, dim3((uint32_t)grid), dim3(512), s, x, w, zb, off, o,
                            (int)a.R, a.N, (int)a.k_cand, (int)a.d_out, tiles_m, (int)slots, step,
                            fr);
     };
