@@ -1,6 +1,7 @@
 """Throughput benchmark of the IKBO hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 5] [--no-cpu-baseline]
+                    [--flush auto|on|off]
     python bench.py --variant NAME     (one operator variant; see variants.py)
 
 A step is one pass of the workload's whole hot path over one batch (default:
@@ -9,6 +10,12 @@ linear 2048+512 -> 1024 with ReLU, linear 1024 -> 256, request-side K/V
 projection of the 2048-row histories, DCA attention with 8 heads x 128). Inputs
 and weights are resident in HBM before timing starts; W untimed steps, then K
 timed steps between device synchronisations. Prints ONE JSON line.
+
+Workloads 1-4 fit in the 256 MiB last-level cache (MALL), so by default a
+512 MiB buffer is written between timed steps (outside the HIP events that
+time each step) and the step time is the median of the per-step event
+times; workload 5 runs its steps back to back and the step time is the wall
+clock over the K steps. Per-operator times are medians over the K steps.
 
 roofline: the kernel with the largest time per step, timed live with HIP
 events recorded on the stream it runs on, against its algorithmic FLOPs (or
@@ -75,8 +82,11 @@ def op_plan(w):
         return [("ikbo_linear", *_linear_work(4, 256, 256, 128, 256, 4), "alu"),
                 ("dca_attention", *_attention_work(256, 1, 2, 32, [(64, 32)] * 4, 4), "alu")]
     if cid == 2:
-        return [("ikbo_linear_l1", *_linear_work(w.n_req, w.n_cand, 1024, 256, 512), "hbm"),
-                ("linear_l2", *_linear_work(0, w.n_cand, 0, 512, 256), "hbm")]
+        # Both layers in one kernel: the hidden layer never reaches HBM.
+        f1, _ = _linear_work(w.n_req, w.n_cand, 1024, 256, 512)
+        f2, _ = _linear_work(0, w.n_cand, 0, 512, 256)
+        byts = 2 * (w.n_cand * 256 + w.n_req * 1024 + 1280 * 512 + 512 * 256 + w.n_cand * 256)
+        return [("ikbo_mlp2", f1 + f2, byts, "mfma")]
     if cid == 3:
         lens = np.diff(np.asarray(w.kv_offsets, dtype=np.int64))
         l_tot = int(lens.sum())
@@ -88,8 +98,12 @@ def op_plan(w):
                 ("dca_attention_l1", *att, "hbm"), ("kv_projection_l2", *kv, "hbm"),
                 ("q_projection_l2", *q2, "hbm"), ("dca_attention_l2", *att, "hbm")]
     if cid == 4:
-        return [("glm_interaction", *_fm_work(w.n_req, w.n_cand, 32, 8, 128), "hbm"),
-                ("ikbo_linear", *_linear_work(w.n_req, w.n_cand, 1024, 320, 512), "hbm")]
+        # The interaction feeds the linear's operand on chip: Y^C never reaches HBM.
+        ff, _ = _fm_work(w.n_req, w.n_cand, 32, 8, 128)
+        fl, _ = _linear_work(w.n_req, w.n_cand, 1024, 320, 512)
+        byts = 2 * (w.n_cand * 8 * 128 + w.n_req * 32 * 128 + w.n_req * 1024
+                    + 1344 * 512 + w.n_cand * 512)
+        return [("glm_fm_linear", ff + fl, byts, "hbm")]
     if cid == 5:
         lens = np.diff(np.asarray(w.kv_offsets, dtype=np.int64))
         return [("ikbo_linear_l1", *_linear_work(w.n_req, w.n_cand, 2048, 512, 1024), "mfma"),
@@ -113,10 +127,7 @@ def timed_step_fns(p):
                 lambda: ops.dca_attention(p.q, p.k, p.v, p.cand_offsets, p.kv_offsets,
                                           out=p.attention)]
     if cid == 2:
-        return [lambda: ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
-                                        cand_offsets=p.cand_offsets, activation="relu",
-                                        out=p.h1, workspace=p.ws),
-                lambda: ops.ikbo_linear(p.h1, p.w2, out=p.out)]
+        return [lambda: pipelines.step(p)]
     if cid == 3:
         def att(q, kv, o):
             k, v = kvv(kv, p.h, p.d)
@@ -130,11 +141,7 @@ def timed_step_fns(p):
                                         out=p.q2),
                 lambda: att(p.q2, p.kv2, p.a2)]
     if cid == 4:
-        return [lambda: ops.glm_interaction(p.x_req, p.x_cand, p.cand_offsets, y_req=p.y_req,
-                                            y_cand=p.y_cand),
-                lambda: ops.ikbo_linear(p.y_cand, p.w_cand, x_req=p.y_req, w_req=p.w_req,
-                                        cand_offsets=p.cand_offsets, activation="relu",
-                                        out=p.out, workspace=p.ws)]
+        return [lambda: pipelines.step(p)]
     if cid == 5:
         def att():
             k, v = kvv(p.kv, p.h, p.d)
@@ -150,6 +157,7 @@ def timed_step_fns(p):
 
 
 _OP_KERNEL = (("dca_attention", "dca_attn_bf16"), ("glm_interaction", "glm_fm_bf16"),
+              ("ikbo_mlp2", "ikbo_mlp2_bf16"), ("glm_fm_linear", "glm_fm_linear_bf16"),
               ("", "ikbo_gemm_stream"))
 
 
@@ -163,20 +171,42 @@ def profiled_traffic(workload, op):
     with open(path) as f:
         rec = json.load(f)
     key = next(k for prefix, k in _OP_KERNEL if op.startswith(prefix))
-    if rec.get("source_sha256") != prof_summary.source_hash(key):
+    if key not in prof_summary.KERNEL_SOURCES or \
+            rec.get("source_sha256") != prof_summary.source_hash(key):
         return None
     return rec["hbm_bytes_per_launch"]
+
+
+def _host_description():
+    """CPU model and the BLAS library NumPy calls (vendor, version, threads)."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas, threads = "unknown", 1
+    try:
+        from threadpoolctl import threadpool_info
+        infos = [t for t in threadpool_info() if t.get("user_api") == "blas"]
+        if infos:
+            t = infos[0]
+            blas = (f"{t.get('internal_api', '?')} {t.get('version', '')} "
+                    f"({t.get('threading_layer', '?')} threads)").strip()
+            threads = max(int(i.get("num_threads", 1)) for i in infos)
+    except Exception:   # noqa: BLE001 - reporting only
+        pass
+    return model, blas, threads
 
 
 def cpu_baseline(w, cid):
     """The oracle, as it stands, on a bounded sample of the workload."""
     import numpy as np
     from oracle import pipelines as op
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([t.get("num_threads", 1) for t in threadpool_info()] or [1])
-    except Exception:   # noqa: BLE001 - reporting only
-        threads = 1
+    model, blas, threads = _host_description()
     cores = min(threads, len(os.sched_getaffinity(0)))
     if cid == 5:
         n_s = 1024
@@ -203,14 +233,16 @@ def cpu_baseline(w, cid):
         total = t_s * w.n_cand / n_s
         sample = f"first {n_s} candidates, extrapolated linearly to {w.n_cand}"
     return {"value": w.n_cand / total, "unit": "candidates/s", "cores": int(cores),
-            "kind": "oracle", "sample": sample}
+            "kind": "oracle", "sample": sample, "cpu": model, "blas": blas}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--flush", choices=["auto", "on", "off"], default="auto",
+                    help="write a 512 MiB buffer between timed steps (auto: workloads 1-4)")
     ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", default=None,
@@ -245,26 +277,34 @@ def main():
     assert len(plan) == len(fns)
 
     stream = torch.cuda.current_stream()
+    flush = args.flush == "on" or (args.flush == "auto" and args.workload != 5)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda") if flush else None
     log(f"warmup x{args.warmup}")
     for _ in range(args.warmup):
         pipelines.step(p)
     torch.cuda.synchronize()
 
-    log(f"timing x{args.steps}")
+    log(f"timing x{args.steps}" + (" (512 MiB written between steps)" if flush else ""))
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in fns] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
+        if flush:
+            scratch.fill_(s & 0xff)       # evicts the previous step's data; outside the events
         for i, fn in enumerate(fns):
             ev[s][i][0].record(stream)
             fn()
             ev[s][i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_step = 1e3 * wall / args.steps
-    op_ms = [float(np.mean([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)]))
-             for i in range(len(fns))]
+    step_ms = [ev[s][0][0].elapsed_time(ev[s][-1][1]) for s in range(args.steps)]
+    # Back-to-back steps: the wall clock over the K steps. With the flush
+    # between steps the wall clock includes it, so the step time is the
+    # median of the per-step event times instead.
+    ms_step = float(np.median(step_ms)) if flush else 1e3 * wall / args.steps
+    op_ms = [float(np.median([ev[s][i][0].elapsed_time(ev[s][i][1])
+                              for s in range(args.steps)])) for i in range(len(fns))]
 
     kernels = {}
     fp32 = w.dtype == "f32"
@@ -300,6 +340,11 @@ def main():
         "unit": "candidates/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "timing": {"step_ms_median_events": round(float(np.median(step_ms)), 4),
+                   "wall_ms_per_step": round(1e3 * wall / args.steps, 4),
+                   "cache_flush_between_steps": flush,
+                   "step_time": "median of per-step HIP events" if flush
+                   else "wall clock over the timed steps"},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32" if fp32 else "bf16", "data": "synthetic",
         "config": {"workload": f"{names[args.workload]}: {wl.WORKLOAD_NAMES[args.workload]}",

@@ -101,13 +101,12 @@ const char* rocs_last_error_message(void);
  * every pointer 16-byte aligned. Other shapes take a slower general kernel
  * (the zero-padding transform of Section 4.2.4 restores the fast path).
  *
- * Environment: ROCS_LINEAR_COMBINED=1 runs the request-side GEMM inside the
- * candidate kernel (one launch, Section 4.2.3) when the streaming candidate
- * kernel applies (k_cand a multiple of 64, no x_cand_add): request tiles
- * first, per-tile completion flags with agent-scope release / acquire. The
- * workspace then also holds the flags (rocs_ikbo_linear_workspace_size
- * covers them). Off by default: on MI355X the cross-XCD L2 write-back and
- * invalidate cost more than the launch saved.
+ * The request-side GEMM is a launch of its own; rocs_ikbo_linear_combined
+ * runs it inside the candidate kernel instead (Section 4.2.3).
+ *
+ * Limits: every size below 2^31. Off the fast path the general kernels run
+ * one thread per output element, so N * d_out must stay below 2^32
+ * (ROCS_ERR_UNSUPPORTED otherwise).
  * ---------------------------------------------------------------------------
  */
 size_t rocs_ikbo_linear_workspace_size(int64_t num_requests, int64_t num_cand,
@@ -151,6 +150,43 @@ int32_t rocs_glm_linear(const void* x_req, int64_t k_req,
                         int64_t num_requests, int64_t num_cand, int64_t d_req, int64_t d_cand,
                         int32_t dtype, int32_t activation, void* y_req, void* y_cand,
                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_ikbo_linear_combined: the outputs of rocs_glm_linear (y_req optional)
+ * from one launch: the combined request + candidate kernel of Section 4.2.3.
+ * The streaming candidate kernel first computes the stacked request GEMM's
+ * 16 x 16 tiles (request tiles in ascending order); each tile of the request
+ * table Z publishes a completion flag with an agent-scope release, and a
+ * workgroup waits for every flag (bounded: past the limit it computes the
+ * missing tiles itself, with the same code and so the same values) while its
+ * first candidate loads are in flight, then takes its candidate tiles in
+ * descending order. The flags live in the workspace, tagged with a per-call
+ * epoch, so nothing needs clearing between calls.
+ *
+ *   Arguments as for rocs_glm_linear, except that y_req may be NULL: then
+ *   w_rr, b_req and d_req are ignored and only y_cand is produced (the
+ *   rocs_ikbo_linear output, with w_cr and w_cc in the roles of w_req and
+ *   w_cand). The workspace is rocs_ikbo_linear_workspace_size(R, N, d_cand,
+ *   k_req) bytes, as for the separate launches.
+ *
+ * The results equal those of rocs_glm_linear / rocs_ikbo_linear bit for bit.
+ * The combined kernel runs where the streaming candidate kernel does (bf16
+ * fast path, k_cand a multiple of 64, no x_cand_add, k_req > 0, N > 0);
+ * other calls run the separate launches. On MI355X the separate launches are
+ * usually faster: the cross-XCD L2 write-back behind each release and the
+ * invalidate behind each acquire cost more than the launch they save.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_ikbo_linear_combined(const void* x_req, int64_t k_req,
+                                  const void* x_cand, const void* x_cand_add, int64_t k_cand,
+                                  const void* w_rr, const void* w_cr, const void* w_cc,
+                                  const float* b_req, const float* b_cand,
+                                  const int32_t* cand_offsets,
+                                  int64_t num_requests, int64_t num_cand, int64_t d_req,
+                                  int64_t d_cand, int32_t dtype, int32_t activation,
+                                  void* y_req, void* y_cand,
+                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * ---------------------------------------------------------------------------
@@ -209,6 +245,11 @@ int32_t rocs_ikbo_linear_mapped(const void* x_req, int64_t k_req,
  * Fast path (bf16 MFMA kernel): bf16, head_dim 64 or 128, H*head_dim and
  * kv_row_stride multiples of 8, pointers 16-byte aligned. Other cases run a
  * general kernel.
+ *
+ * Limits: N * q_len below 2^31 and num_heads below 2^16. The general kernel
+ * runs one wave per query row and head, so it takes N * q_len below 2^26;
+ * the fast path takes (R + N * q_len / 128) * num_heads below 2^24. Larger
+ * calls return ROCS_ERR_UNSUPPORTED.
  * ---------------------------------------------------------------------------
  */
 int32_t rocs_dca_attention(const void* q, const void* k, const void* v,

@@ -23,6 +23,9 @@ SIGNATURES = {
                                 _i64, _i64, _i64, _i32, _i32, _vp, _vp, _size, _vp]),
     "rocs_glm_linear": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp,
                                _i64, _i64, _i64, _i64, _i32, _i32, _vp, _vp, _vp, _size, _vp]),
+    "rocs_ikbo_linear_combined": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
+                                         _vp, _i64, _i64, _i64, _i64, _i32, _i32, _vp, _vp, _vp,
+                                         _size, _vp]),
     "rocs_ikbo_linear_mapped": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                        _i64, _i64, _i64, _i32, _i32, _vp, _vp, _size, _vp]),
     "rocs_dca_attention": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32,

@@ -3,7 +3,6 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
-#include <cstdlib>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -29,6 +28,15 @@ int32_t fail(rocs_status s, const char* fmt, ...) {
 int32_t ok() {
   g_error.clear();
   return ROCS_OK;
+}
+
+// A launcher's error: a grid too large for one launch (the launchers test
+// their computed grids before narrowing them) is a shape this build does not
+// run; anything else is the runtime's refusal.
+int32_t launch_failed(const char* name, hipError_t e) {
+  if (e == hipErrorInvalidConfiguration)
+    return fail(ROCS_ERR_UNSUPPORTED, "%s: the launch grid would exceed 2^32 work items", name);
+  return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
 }
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
@@ -98,7 +106,7 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
                     const int32_t* cand_offsets, const int32_t* cand_ids, int64_t R, int64_t N,
                     int64_t d_out, int32_t dtype, int32_t activation, void* out,
                     void* workspace, size_t workspace_bytes, void* stream,
-                    const RequestSide& rs = RequestSide()) {
+                    const RequestSide& rs = RequestSide(), bool combined = false) {
   const bool full = rs.y_req != nullptr;
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (activation != ROCS_ACT_NONE && activation != ROCS_ACT_RELU)
@@ -184,8 +192,7 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
   a.relu = activation == ROCS_ACT_RELU;
   a.out = out;
   a.w_rr = rs.w_rr; a.b_rr = rs.b_rr; a.y_req = rs.y_req; a.d_req = rs.d_req;
-  const char* combined = getenv("ROCS_LINEAR_COMBINED");
-  a.combined = combined != nullptr && combined[0] == '1';
+  a.combined = combined;
   if (need > 0) {
     a.z = static_cast<float*>(workspace);
     a.ids = mapped ? const_cast<int32_t*>(cand_ids)
@@ -199,8 +206,15 @@ int32_t linear_impl(const char* name, bool mapped, const void* x_req, int64_t k_
                     aligned(out, 16) &&
                     (!full || (rs.d_req % 4 == 0 && aligned(rs.w_rr, 16) &&
                                aligned(rs.b_rr, 16) && aligned(rs.y_req, 8)));
+  // The general kernels run one thread per output element (and the request
+  // kernel one per request-side element); keep their grids under 2^32 items.
+  if (!fast && ((N * d_out) >> 32 != 0 || (R * (d_out + (full ? rs.d_req : 0))) >> 32 != 0 ||
+                (full && (R * rs.d_req) >> 32 != 0)))
+    return fail(ROCS_ERR_UNSUPPORTED, "%s: the general kernel's grid would exceed 2^32 threads "
+                "(N * d_out = %lld); the bf16 fast path has no such limit", name,
+                (long long)(N * d_out));
   const hipError_t e = rocs::launch_linear(a, fast, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
+  if (e != hipSuccess) return launch_failed(name, e);
   return ok();
 }
 
@@ -231,6 +245,22 @@ int32_t rocs_glm_linear(const void* x_req, int64_t k_req, const void* x_cand,
   return linear_impl("rocs_glm_linear", false, x_req, k_req, x_cand, x_cand_add, k_cand, w_cr,
                      w_cc, b_cand, cand_offsets, nullptr, R, N, d_cand, dtype, activation,
                      y_cand, workspace, workspace_bytes, stream, rs);
+}
+
+int32_t rocs_ikbo_linear_combined(const void* x_req, int64_t k_req, const void* x_cand,
+                                  const void* x_cand_add, int64_t k_cand, const void* w_rr,
+                                  const void* w_cr, const void* w_cc, const float* b_req,
+                                  const float* b_cand, const int32_t* cand_offsets, int64_t R,
+                                  int64_t N, int64_t d_req, int64_t d_cand, int32_t dtype,
+                                  int32_t activation, void* y_req, void* y_cand,
+                                  void* workspace, size_t workspace_bytes, void* stream) {
+  RequestSide rs;
+  if (y_req != nullptr) {
+    rs.w_rr = w_rr; rs.b_rr = b_req; rs.y_req = y_req; rs.d_req = d_req;
+  }
+  return linear_impl("rocs_ikbo_linear_combined", false, x_req, k_req, x_cand, x_cand_add,
+                     k_cand, w_cr, w_cc, b_cand, cand_offsets, nullptr, R, N, d_cand, dtype,
+                     activation, y_cand, workspace, workspace_bytes, stream, rs, true);
 }
 
 int32_t rocs_ikbo_linear_mapped(const void* x_req, int64_t k_req, const void* x_cand,
@@ -293,8 +323,18 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
   const bool fast = a.bf16 && (head_dim == 64 || head_dim == 128) && stride % 8 == 0 &&
                     stride < (int64_t(1) << 24) &&
                     aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16);
+  // Launch limits: a grid may hold fewer than 2^32 work items. The general
+  // kernel runs one 64-lane wave per (query row, head) with the rows on the
+  // grid's x axis; the tiled kernel (CSR only) runs 256 lanes per (head,
+  // tile slot), R + ceil(N q_len / 128) slots per head.
+  if ((!fast || mapped) && (N * q_len) >= (int64_t(1) << 26))
+    return fail(ROCS_ERR_UNSUPPORTED, "%s: N * q_len = %lld query rows exceed the general "
+                "kernel's grid (2^26 rows)", name, (long long)(N * q_len));
+  if (fast && !mapped && (R + (N * q_len + 127) / 128) * num_heads >= (int64_t(1) << 24))
+    return fail(ROCS_ERR_UNSUPPORTED, "%s: (R + N * q_len / 128) * num_heads tiles exceed the "
+                "grid limit (2^24)", name);
   const hipError_t e = rocs::launch_attention(a, fast, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
+  if (e != hipSuccess) return launch_failed(name, e);
   return ok();
 }
 
@@ -357,7 +397,7 @@ int32_t rocs_glm_interaction(const void* x_req, const void* x_cand, const int32_
                     aligned(y_req, 16) && aligned(y_cand, 16);
   const hipError_t e = rocs::launch_interaction(a, fast, static_cast<hipStream_t>(stream));
   if (e != hipSuccess)
-    return fail(ROCS_ERR_HIP, "rocs_glm_interaction: %s", hipGetErrorString(e));
+    return launch_failed("rocs_glm_interaction", e);
   return ok();
 }
 
@@ -431,7 +471,7 @@ int32_t lcb_impl(const char* name, bool mapped, const void* x_req, const void* x
                     aligned(w_cc, 8) && aligned(y_cand, 16) && aligned(x_req, 8) &&
                     aligned(y_req, 8);
   const hipError_t e = rocs::launch_lcb(a, fast, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "%s: %s", name, hipGetErrorString(e));
+  if (e != hipSuccess) return launch_failed(name, e);
   return ok();
 }
 
@@ -573,7 +613,7 @@ int32_t rocs_ikbo_mlp2(const void* x_req, int64_t k_req, const void* x_cand, int
                     aligned(w2, 16) && aligned(b2, 16) && aligned(out, 16);
   }
   const hipError_t e = rocs::launch_mlp2(a, fused, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_ikbo_mlp2: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return launch_failed("rocs_ikbo_mlp2", e);
   return ok();
 }
 
@@ -673,7 +713,7 @@ int32_t rocs_glm_fm_linear(const void* x_req, const void* x_cand, const int32_t*
                   aligned(w_req, 16) && aligned(w_cand, 16) && aligned(bias, 16) &&
                   aligned(out, 16);
   const hipError_t e = rocs::launch_fm_linear(a, fused, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_glm_fm_linear: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return launch_failed("rocs_glm_fm_linear", e);
   return ok();
 }
 
@@ -687,7 +727,7 @@ int32_t rocs_request_ids(const int32_t* cand_offsets, int64_t R, int64_t N, int3
     return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
   const hipError_t e = rocs::launch_request_ids(cand_offsets, R, N, out_ids,
                                                 static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(ROCS_ERR_HIP, "rocs_request_ids: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return launch_failed("rocs_request_ids", e);
   return ok();
 }
 

@@ -27,13 +27,17 @@ namespace rocs {
 namespace {
 
 constexpr int kTileKeys = 64;    // history rows per K/V stage
-// Online softmax bound: a stage's weights are kept only while their per-lane
-// sum is at most 2^64 (each weight then is too); otherwise the running max
-// moves to the stage max. Row sums stay below L * 2^64 and outputs below
-// L * 2^64 * max|v|, finite in fp32 (and in bf16, which has its exponent
-// range) for any realistic history.
+// Online softmax bound. A stage's weights, taken against the running max as
+// it stands, are accepted as they are while their per-lane sum is at most
+// 2^64. Otherwise the stage takes its row max, and the running max moves to
+// it only if it lies more than kLazyRescale above the running max; either
+// way every accepted weight is then at most 2^64 (it may sit just under the
+// bound on all 32 keys of a lane, so an accepted per-lane stage sum is at
+// most 32 * 2^64). Row sums therefore stay below L * 2^64 and outputs below
+// L * 2^64 * max|v|: finite in fp32 (and in bf16, which has fp32's exponent
+// range) for any history shorter than 2^60 rows.
 constexpr float kLazyRescale = 64.0f;     // log2 of the largest unnormalised weight
-constexpr float kWeightBound = 0x1p64f;
+constexpr float kWeightBound = 0x1p64f;   // per-lane stage sum accepted without a row max
 
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel (32x32x16 shape), head_dim D in {64, 128}.
@@ -486,6 +490,7 @@ hipError_t launch_fast(const AttentionArgs& a, hipStream_t s) {
   const int64_t slots = a.R + (a.N * a.q_len + TR - 1) / TR;
   const int64_t grid = slots * a.heads;
   const float scale_log2 = a.scale * 1.4426950408889634f;
+  if (!grid_fits(grid, 64 * W)) return hipErrorInvalidConfiguration;
   return launch_kernel(dca_attn_bf16<D, W>, dim3((uint32_t)grid), dim3(64 * W), s,
                        static_cast<const bf16_t*>(a.q), static_cast<const bf16_t*>(a.k),
                        static_cast<const bf16_t*>(a.v), a.cand_offsets, a.kv_offsets,
@@ -495,6 +500,7 @@ hipError_t launch_fast(const AttentionArgs& a, hipStream_t s) {
 
 template <typename T>
 hipError_t launch_generic(const AttentionArgs& a, hipStream_t s) {
+  if (!grid_fits(a.N * a.q_len, 64) || a.heads > 65535) return hipErrorInvalidConfiguration;
   return launch_kernel(dca_attn_generic<T>, dim3((uint32_t)(a.N * a.q_len), (uint32_t)a.heads),
                        dim3(64), s, static_cast<const T*>(a.q), static_cast<const T*>(a.k),
                        static_cast<const T*>(a.v), a.cand_offsets, a.kv_offsets,

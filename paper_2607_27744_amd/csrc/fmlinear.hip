@@ -273,6 +273,7 @@ hipError_t launch_fm_linear(const FmLinearArgs& a, bool fused, hipStream_t s) {
   e = launch_request_table(l, s);
   if (e != hipSuccess) return e;
   const int64_t slots = a.R + (a.N + kFlBM - 1) / kFlBM;
+  if (!grid_fits(slots, 256)) return hipErrorInvalidConfiguration;
   return launch_kernel(glm_fm_linear_bf16, dim3((uint32_t)slots), dim3(256), s,
                        static_cast<const bf16_t*>(a.x_req), static_cast<const bf16_t*>(a.x_cand),
                        static_cast<const float*>(a.z), static_cast<const bf16_t*>(a.w_cand),

@@ -134,6 +134,7 @@ __global__ __launch_bounds__(256) void glm_fm_cand_generic(const T* __restrict__
 template <int FC>
 hipError_t launch_fast(const InteractionArgs& a, hipStream_t s) {
   const int64_t slots = a.R + (a.N * FC + kFmRows - 1) / kFmRows;
+  if (!grid_fits(slots, 256)) return hipErrorInvalidConfiguration;
   return launch_kernel(glm_fm_bf16<FC>, dim3((uint32_t)slots), dim3(256), s,
                        static_cast<const bf16_t*>(a.x_req), static_cast<const bf16_t*>(a.x_cand),
                        a.cand_offsets, static_cast<bf16_t*>(a.y_req),
@@ -145,6 +146,7 @@ hipError_t launch_generic(const InteractionArgs& a, hipStream_t s) {
   hipError_t e = hipSuccess;
   if (a.y_req != nullptr) {
     const int64_t n = a.R * a.f_req * a.f_req;
+    if (!grid_fits((n + 255) / 256, 256)) return hipErrorInvalidConfiguration;
     e = launch_kernel(glm_fm_request_generic<T>, dim3((uint32_t)((n + 255) / 256)), dim3(256), s,
                       static_cast<const T*>(a.x_req), static_cast<T*>(a.y_req), a.R, a.f_req,
                       a.emb);
@@ -152,6 +154,7 @@ hipError_t launch_generic(const InteractionArgs& a, hipStream_t s) {
   }
   if (a.y_cand != nullptr && a.N > 0) {
     const int64_t n = a.N * a.f_cand * (a.f_req + a.f_cand);
+    if (!grid_fits((n + 255) / 256, 256)) return hipErrorInvalidConfiguration;
     e = launch_kernel(glm_fm_cand_generic<T>, dim3((uint32_t)((n + 255) / 256)), dim3(256), s,
                       static_cast<const T*>(a.x_req), static_cast<const T*>(a.x_cand),
                       a.cand_offsets, static_cast<T*>(a.y_cand), (int)a.R, a.N, a.f_req,

@@ -274,9 +274,8 @@ __global__ __launch_bounds__(256) void lcb_cand_generic(
 
 template <int NK, int E, int NOB>
 hipError_t launch_cand_fast(const LcbArgs& a, hipStream_t s) {
-  int dev = 0, cus = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  int cus = 0;
+  const hipError_t e = current_cu_count(&cus);
   if (e != hipSuccess) return e;
   // Runs of at least 4 candidates per wave, about eight waves per CU at once.
   const int64_t waves_target = (int64_t)cus * 8;
@@ -337,12 +336,14 @@ hipError_t launch_typed(const LcbArgs& a, bool fast, hipStream_t s) {
   if (std::is_same_v<T, bf16_t> && fast) {
     // fast implies E in {64, 128} and 16-byte aligned rows
     const int64_t req_threads = a.R * (int64_t)(a.o_req + a.o_cand) * (a.emb / 4);
+    if (!grid_fits((req_threads + 255) / 256, 256)) return hipErrorInvalidConfiguration;
     e = launch_kernel(lcb_request_bf16x4, dim3((uint32_t)((req_threads + 255) / 256)), dim3(256),
                       s, static_cast<const bf16_t*>(a.x_req), static_cast<const bf16_t*>(a.w_rr),
                       static_cast<const bf16_t*>(a.w_cr), static_cast<bf16_t*>(a.y_req), a.z,
                       (int)a.R, a.f_req, a.o_req, a.o_cand, a.emb);
   } else {
     const int64_t req_elems = a.R * (int64_t)(a.o_req + a.o_cand) * a.emb;
+    if (!grid_fits((req_elems + 255) / 256, 256)) return hipErrorInvalidConfiguration;
     e = launch_kernel(lcb_request<T>, dim3((uint32_t)((req_elems + 255) / 256)), dim3(256),
                       s, static_cast<const T*>(a.x_req), static_cast<const T*>(a.w_rr),
                       static_cast<const T*>(a.w_cr), static_cast<T*>(a.y_req), a.z,
@@ -356,6 +357,7 @@ hipError_t launch_typed(const LcbArgs& a, bool fast, hipStream_t s) {
     }
   }
   const int64_t cand_elems = a.N * (int64_t)a.o_cand * a.emb;
+  if (!grid_fits((cand_elems + 255) / 256, 256)) return hipErrorInvalidConfiguration;
   return launch_kernel(lcb_cand_generic<T>, dim3((uint32_t)((cand_elems + 255) / 256)), dim3(256),
                        s, static_cast<const T*>(a.x_cand), static_cast<const T*>(a.w_cc), a.z,
                        a.cand_offsets, a.ids, static_cast<T*>(a.y_cand), (int)a.R, a.N, a.f_cand,

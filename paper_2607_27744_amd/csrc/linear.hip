@@ -794,6 +794,7 @@ hipError_t launch_fast_gemm(const LinearArgs& a, hipStream_t s) {
   const int tiles_m = (int)((a.d_out + BM - 1) / BM);
   const int64_t tiles_n = (a.N + BN - 1) / BN;
   const int64_t grid = tiles_m * tiles_n;
+  if (!grid_fits(grid, 64 * WMW * WNW)) return hipErrorInvalidConfiguration;
   const bf16_t* x = static_cast<const bf16_t*>(a.x_cand);
   const bf16_t* xa = static_cast<const bf16_t*>(a.x_cand_add);
   const bf16_t* w = static_cast<const bf16_t*>(a.w_cand);
@@ -814,6 +815,8 @@ template <typename T>
 hipError_t launch_generic(const LinearArgs& a, hipStream_t s) {
   hipError_t e = hipSuccess;
   if (a.k_req > 0) {
+    if (!grid_fits((a.R * a.d_out + 255) / 256 + (a.N + 255) / 256, 256))
+      return hipErrorInvalidConfiguration;
     const int z_blocks = (int)((a.R * a.d_out + 255) / 256);
     const int id_blocks = a.ids_given ? 0 : (int)((a.N + 255) / 256);
     e = launch_kernel(request_gemm_generic<T>, dim3(z_blocks + id_blocks), dim3(256), s,
@@ -823,6 +826,7 @@ hipError_t launch_generic(const LinearArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   const int64_t blocks = (a.N * a.d_out + 255) / 256;
+  if (!grid_fits(blocks, 256)) return hipErrorInvalidConfiguration;
   return launch_kernel(linear_generic<T>, dim3((uint32_t)blocks), dim3(256), s,
                        static_cast<const T*>(a.x_cand), static_cast<const T*>(a.x_cand_add),
                        static_cast<const T*>(a.w_cand), a.bias,
@@ -834,12 +838,14 @@ hipError_t launch_generic(const LinearArgs& a, hipStream_t s) {
 
 hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t* ids,
                               hipStream_t s) {
+  if (!grid_fits((N + 255) / 256, 256)) return hipErrorInvalidConfiguration;
   return launch_kernel(request_ids_kernel, dim3((uint32_t)((N + 255) / 256)), dim3(256), s,
                        off, (int)R, N, ids);
 }
 
 hipError_t launch_request_table(const LinearArgs& a, hipStream_t s) {
   const int tiles_d = (int)((a.d_out + 15) / 16);
+  if (!grid_fits((int64_t)tiles_d * ((a.R + 15) / 16), 256)) return hipErrorInvalidConfiguration;
   const int req_tiles = tiles_d * (int)((a.R + 15) / 16);
   const RequestOut none{nullptr, nullptr, nullptr, 0, 0, 0};
   return launch_kernel(request_gemm_bf16, dim3(req_tiles), dim3(256), s,
@@ -879,6 +885,9 @@ hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
                 (int)a.d_req, a.y_req != nullptr ? (int)((a.d_req + 15) / 16) : 0, (int)a.relu};
   // No candidates: only the Y^R tiles (the request table has no reader).
   const int tiles_d = a.N > 0 ? (int)((a.d_out + 15) / 16) : 0;
+  if (a.k_req > 0 && !grid_fits((int64_t)(yr.tiles + tiles_d) * ((a.R + 15) / 16) +
+                                    (a.N + 255) / 256, 256))
+    return hipErrorInvalidConfiguration;
   const int req_tiles = (yr.tiles + tiles_d) * (int)((a.R + 15) / 16);
   if (a.k_req > 0 && !fused) {
     const int id_blocks = stream || a.ids_given ? 0 : (int)((a.N + 255) / 256);
@@ -894,9 +903,8 @@ hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s) {
     const int tiles_m = (int)((a.d_out + kStreamBM - 1) / kStreamBM);
     const int64_t slots = (a.k_req > 0 ? a.R : 0) + (a.N + kStreamBN - 1) / kStreamBN;
     const int64_t n_tiles = slots * tiles_m;
-    int dev = 0, cus = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    int cus = 0;
+    const hipError_t e = current_cu_count(&cus);
     if (e != hipSuccess) return e;
     const int grid = (int)(n_tiles < cus ? n_tiles : cus);
     const StreamStep step{grid / tiles_m, grid % tiles_m};

@@ -352,9 +352,8 @@ void ikbo_mlp2_bf16(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
 template <int KC, int DO>
 hipError_t launch_fused(const Mlp2Args& a, const float* zb, int64_t zb_stride,
                         const int32_t* off, hipStream_t s) {
-  int dev = 0, cus = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  int cus = 0;
+  const hipError_t e = current_cu_count(&cus);
   if (e != hipSuccess) return e;
   const int64_t tiles = (a.N + kMlpBM - 1) / kMlpBM;
   const int grid = (int)(tiles < cus ? tiles : cus);

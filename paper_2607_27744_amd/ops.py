@@ -14,7 +14,8 @@ import torch
 from . import _lib
 
 __all__ = [
-    "load_library", "ikbo_linear", "ikbo_linear_mapped", "glm_linear", "linear_workspace_size",
+    "load_library", "ikbo_linear", "ikbo_linear_mapped", "glm_linear", "ikbo_linear_combined",
+    "linear_workspace_size", "pad_dims",
     "dca_attention", "dca_attention_mapped", "dca_request_attention", "glm_interaction",
     "ikbo_lcb", "ikbo_lcb_mapped", "ikbo_mlp2", "mlp2_workspace_size", "glm_fm_linear",
     "fm_linear_workspace_size", "request_ids",
@@ -97,6 +98,57 @@ def ikbo_linear_mapped(x_cand, w_cand, *, x_req=None, w_req=None, cand_request_i
                    activation, x_cand_add, out, workspace, stream)
 
 
+def pad_dims(x, w, multiple=64):
+    """The memory-alignment transform (Section 4.2.4): zero-pad the reduction
+    width K of an activation x [rows, K] and of its weight w [D, K] up to a
+    multiple of `multiple`. The added columns are zero on both sides, so
+    x @ w.T is unchanged; the padded shapes reach the aligned kernels (K a
+    multiple of 64 for the streaming candidate GEMM, 8 for the request GEMM).
+    Layout only: returns (x, w) unchanged when K is already a multiple, else
+    zero-padded copies (pad weights once, ahead of the calls that use them)."""
+    _need(x.dim() == 2 and w.dim() == 2 and x.shape[1] == w.shape[1],
+          "x [rows, K] and w [D, K] expected")
+    _need(multiple >= 1, "multiple must be positive")
+    k = x.shape[1]
+    pad = (-k) % multiple
+    if pad == 0:
+        return x, w
+    xp = torch.zeros((x.shape[0], k + pad), dtype=x.dtype, device=x.device)
+    wp = torch.zeros((w.shape[0], k + pad), dtype=w.dtype, device=w.device)
+    xp[:, :k] = x
+    wp[:, :k] = w
+    return xp, wp
+
+
+def ikbo_linear_combined(x_req, x_cand, w_cr, w_cc, cand_offsets, *, w_rr=None, b_req=None,
+                         b_cand=None, activation="none", x_cand_add=None, y_req=None,
+                         y_cand=None, workspace=None, stream=None):
+    """rocs_ikbo_linear_combined: the request-side GEMM and the candidate GEMM in
+    one launch (Section 4.2.3). Returns (y_req or None, y_cand); y_req =
+    act(W_RR x^R + b^R) when w_rr is given. Results equal glm_linear /
+    ikbo_linear bit for bit."""
+    lib = _lib.load()
+    _need(x_req is not None and x_req.dim() == 2, "x_req must be [R, k_req]")
+    n_req, k_req = x_req.shape
+    side = None
+    if w_rr is not None:
+        _need(w_rr.dim() == 2 and w_rr.shape[1] == k_req, "w_rr must be [d_req, k_req]")
+        d_req = w_rr.shape[0]
+        _need(w_rr.dtype == x_req.dtype and w_rr.is_contiguous(), "w_rr must match x_req")
+        if b_req is not None:
+            _need(b_req.dtype == torch.float32 and b_req.shape == (d_req,),
+                  "b_req must be float32 [d_req]")
+        if y_req is None:
+            y_req = torch.empty((n_req, d_req), dtype=x_req.dtype, device=x_req.device)
+        _need(y_req.shape == (n_req, d_req) and y_req.dtype == x_req.dtype and
+              y_req.is_contiguous(), "y_req must be a contiguous [R, d_req] tensor")
+        _on_gpu(w_rr, b_req, y_req)
+        side = (w_rr, b_req, y_req, d_req, lib)
+    y_cand = _linear(x_cand, w_cc, x_req, w_cr, cand_offsets, None, None, b_cand, activation,
+                     x_cand_add, y_cand, workspace, stream, request_side=side, combined=True)
+    return y_req, y_cand
+
+
 def glm_linear(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets, *, b_req=None, b_cand=None,
                activation="none", x_cand_add=None, y_req=None, y_cand=None, workspace=None,
                stream=None):
@@ -122,7 +174,7 @@ def glm_linear(x_req, x_cand, w_rr, w_cr, w_cc, cand_offsets, *, b_req=None, b_c
 
 
 def _linear(x_cand, w_cand, x_req, w_req, cand_offsets, cand_ids, mapped, bias, activation,
-            x_cand_add, out, workspace, stream, request_side=None):
+            x_cand_add, out, workspace, stream, request_side=None, combined=False):
     lib = _lib.load()
     _need(x_cand.dim() == 2 and w_cand.dim() == 2, "x_cand and w_cand must be 2-D")
     n_cand, k_cand = x_cand.shape
@@ -162,6 +214,14 @@ def _linear(x_cand, w_cand, x_req, w_req, cand_offsets, cand_ids, mapped, bias, 
     _on_gpu(x_cand, w_cand, x_req, w_req, index, bias, x_cand_add, out, workspace)
     _need(activation in _ACT, f"activation must be one of {sorted(k for k in _ACT if k)}")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if combined:
+        w_rr, b_req, y_req, d_req = (request_side or (None, None, None, 0, None))[:4]
+        _lib.check(lib.rocs_ikbo_linear_combined(
+            _ptr(x_req), k_req, _ptr(x_cand), _ptr(x_cand_add), k_cand, _ptr(w_rr), _ptr(w_req),
+            _ptr(w_cand), _ptr(b_req), _ptr(bias), _ptr(cand_offsets), n_req, n_cand, d_req,
+            d_out, code, _ACT[activation], _ptr(y_req), _ptr(out), _ptr(workspace), ws_bytes,
+            _stream(stream)), "rocs_ikbo_linear_combined")
+        return out
     if request_side is not None:
         w_rr, b_req, y_req, d_req, _ = request_side
         _lib.check(lib.rocs_glm_linear(

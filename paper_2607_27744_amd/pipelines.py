@@ -47,12 +47,13 @@ def prepare(w, device="cuda"):
         p.attention = torch.empty_like(p.q)
         p.ws = _ws(w.n_req, w.n_cand, 256, 256, dev)
     elif cid == 2:
+        # Both layers in one kernel (rocs_ikbo_mlp2): the hidden layer stays on chip.
         p.x_req, p.x_cand = _bf16(w.x_req, dev), _bf16(w.x_cand, dev)
         p.w1_req, p.w1_cand, p.w2 = (_bf16(w.w1_req, dev), _bf16(w.w1_cand, dev),
                                      _bf16(w.w2, dev))
-        p.h1 = torch.empty((w.n_cand, 512), dtype=torch.bfloat16, device=dev)
         p.out = torch.empty((w.n_cand, 256), dtype=torch.bfloat16, device=dev)
-        p.ws = _ws(w.n_req, w.n_cand, 512, 1024, dev)
+        need = ops.mlp2_workspace_size(w.n_req, w.n_cand, 1024, 256, 512, 256, torch.bfloat16)
+        p.ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
     elif cid == 3:
         h, d = w.n_heads, w.head_dim
         p.kv_offsets = _i32(w.kv_offsets, dev)
@@ -69,13 +70,16 @@ def prepare(w, device="cuda"):
         p.a2 = torch.empty_like(p.a1)
         p.h, p.d = h, d
     elif cid == 4:
+        # The interaction fused into the linear's operand (rocs_glm_fm_linear):
+        # Y^C never reaches HBM; the workspace holds Y^R at its start.
         p.x_req, p.x_cand = _bf16(w.x_req, dev), _bf16(w.x_cand, dev)
         p.w_req, p.w_cand = _bf16(w.w_req, dev), _bf16(w.w_cand, dev)
-        p.y_req = torch.empty((w.n_req, w.f_req * w.f_req), dtype=torch.bfloat16, device=dev)
-        p.y_cand = torch.empty((w.n_cand, w.f_cand * (w.f_req + w.f_cand)),
-                               dtype=torch.bfloat16, device=dev)
         p.out = torch.empty((w.n_cand, 512), dtype=torch.bfloat16, device=dev)
-        p.ws = _ws(w.n_req, w.n_cand, 512, w.f_req * w.f_req, dev)
+        need = ops.fm_linear_workspace_size(w.n_req, w.n_cand, w.f_req, w.f_cand, w.emb_dim, 512,
+                                            torch.bfloat16)
+        p.ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        k_r = w.f_req * w.f_req
+        p.y_req = p.ws[:w.n_req * k_r * 2].view(torch.bfloat16).view(w.n_req, k_r)
     elif cid == 5:
         h, d = w.n_heads, w.head_dim
         p.kv_offsets = _i32(w.kv_offsets, dev)
@@ -108,10 +112,9 @@ def step(p):
                         workspace=p.ws)
         ops.dca_attention(p.q, p.k, p.v, p.cand_offsets, p.kv_offsets, out=p.attention)
     elif cid == 2:
-        ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
-                        cand_offsets=p.cand_offsets, activation="relu", out=p.h1,
-                        workspace=p.ws)
-        ops.ikbo_linear(p.h1, p.w2, out=p.out)
+        ops.ikbo_mlp2(p.x_cand, p.w1_cand, p.w2, x_req=p.x_req, w1_req=p.w1_req,
+                      cand_offsets=p.cand_offsets, activation1="relu", activation2="none",
+                      out=p.out, workspace=p.ws)
     elif cid == 3:
         n = p.n_cand
         ops.ikbo_linear(p.s, p.wkv1, out=p.kv1)
@@ -125,10 +128,8 @@ def step(p):
         ops.dca_attention(p.q2.view(n, 1, p.h, p.d), k2, v2, p.cand_offsets, p.kv_offsets,
                           out=p.a2)
     elif cid == 4:
-        ops.glm_interaction(p.x_req, p.x_cand, p.cand_offsets, y_req=p.y_req, y_cand=p.y_cand)
-        ops.ikbo_linear(p.y_cand, p.w_cand, x_req=p.y_req, w_req=p.w_req,
-                        cand_offsets=p.cand_offsets, activation="relu", out=p.out,
-                        workspace=p.ws)
+        ops.glm_fm_linear(p.x_req, p.x_cand, p.cand_offsets, p.w_req, p.w_cand,
+                          activation="relu", out=p.out, workspace=p.ws)
     elif cid == 5:
         n = p.n_cand
         ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
@@ -146,10 +147,10 @@ def outputs(p):
     """Final outputs of the pipeline (name -> device tensor)."""
     return {
         1: lambda: {"linear": p.linear, "attention": p.attention},
-        2: lambda: {"h1": p.h1, "out": p.out},
+        2: lambda: {"out": p.out},
         3: lambda: {"q1": p.q1, "a1": p.a1.view(p.n_cand, -1), "q2": p.q2,
                     "a2": p.a2.view(p.n_cand, -1)},
-        4: lambda: {"y_req": p.y_req, "y_cand": p.y_cand, "out": p.out},
+        4: lambda: {"y_req": p.y_req, "out": p.out},
         5: lambda: {"h1": p.h1, "out2": p.out2, "attention": p.attention.view(p.n_cand, -1)},
     }[p.config_id]()
 

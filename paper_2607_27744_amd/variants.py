@@ -19,7 +19,7 @@ line with the call's algorithmic FLOPs and bytes against the MI355X peaks.
                     candidates, 1024+256 -> 512, ReLU) with the candidates
                     shuffled and m given per candidate
   linear_combined   the same layer with the request side inside the candidate
-                    kernel (ROCS_LINEAR_COMBINED=1), timed beside the two-launch
+                    kernel (rocs_ikbo_linear_combined), timed beside the two-launch
                     form on the same inputs
   glm_linear        the production-scale first layer as a full GLM layer
                     (request output 2048 -> 1024 as well)
@@ -35,7 +35,6 @@ line with the call's algorithmic FLOPs and bytes against the MI355X peaks.
                     ReLU) as one fused call, timed beside the two operators
 """
 
-import os
 
 import numpy as np
 import torch
@@ -178,11 +177,9 @@ def _linear_combined(steps, warmup):
               workspace=torch.zeros(ops.linear_workspace_size(64, n, 512, 1024),
                                     dtype=torch.uint8, device="cuda"))
     ms_sep = _time(lambda: ops.ikbo_linear(*args, **kw), steps, warmup)
-    os.environ["ROCS_LINEAR_COMBINED"] = "1"
-    try:
-        ms = _time(lambda: ops.ikbo_linear(*args, **kw), steps, warmup)
-    finally:
-        del os.environ["ROCS_LINEAR_COMBINED"]
+    ms = _time(lambda: ops.ikbo_linear_combined(
+        kw["x_req"], args[0], kw["w_req"], args[1], kw["cand_offsets"], activation="relu",
+        y_cand=kw["out"], workspace=kw["workspace"]), steps, warmup)
     flops = 2.0 * n * 256 * 512 + 2.0 * 64 * 1024 * 512
     byts = 2.0 * (n * 256 + n * 512 + 1280 * 512 + 64 * 1024)
     return _line("linear_combined", {"requests": 64, "candidates": n, "k_req": 1024,

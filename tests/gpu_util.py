@@ -41,3 +41,19 @@ def assert_close(got, want, what="", atol=ATOL, rtol=RTOL, normwise=NORMWISE):
         rel = np.linalg.norm(got - want) / denom
         assert rel <= normwise, f"{what}: normwise relative error {rel:.3g} > {normwise}"
     return float(err.max()) if err.size else 0.0
+
+
+def tile_rows(off, seed, block=128):
+    """One random row of every `block`-row block of every request, plus the
+    request's first and last row, sorted."""
+    rng = np.random.default_rng(seed)
+    rows = []
+    for r in range(len(off) - 1):
+        a, b = int(off[r]), int(off[r + 1])
+        if b == a:
+            continue
+        starts = np.arange(a, b, block)
+        ends = np.minimum(starts + block, b)
+        rows.extend(rng.integers(starts, ends).tolist())
+        rows.extend([a, b - 1])
+    return np.array(sorted(set(rows)), dtype=np.int64)

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 19
+    assert len(names) == 20
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -264,3 +264,43 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(_lib, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         _lib.load(str(tmp_path / "librocs.so"))
+
+
+FAR = [P((i + 1) << 44) for i in range(12)]    # fake, far apart: huge sizes never overlap
+
+
+@no_gpu
+def test_combined_entry_point_argument_errors(lib):
+    def call(**kw):
+        a = dict(x_req=FAKE[0], k_req=8, x_cand=FAKE[1], x_add=None, k_cand=64, w_rr=None,
+                 w_cr=FAKE[2], w_cc=FAKE[3], b_req=None, b_cand=None, off=FAKE[4], R=2, N=16,
+                 d_req=0, d_cand=8, dtype=1, act=1, y_req=None, y_cand=FAKE[5], ws=FAKE[6],
+                 ws_bytes=1 << 20, stream=None)
+        a.update(kw)
+        return lib.rocs_ikbo_linear_combined(*a.values())
+    assert call(off=None) == _lib.INVALID_ARGUMENT
+    assert call(ws_bytes=16) == _lib.WORKSPACE_TOO_SMALL
+    # y_req given: W_RR is required.
+    assert call(y_req=FAKE[7], d_req=8) == _lib.INVALID_ARGUMENT
+    assert call(N=0) == _lib.OK
+
+
+@no_gpu
+def test_grid_limits_are_unsupported(lib):
+    # The general kernels run one thread (or wave) per output element or
+    # query row; grids of 2^32 work items or more are refused up front.
+    n = 1 << 30
+    st = lib.rocs_ikbo_linear(None, 0, FAR[0], None, 8, None, FAR[1], None, None, 0, n, 8,
+                              0, 0, FAR[2], None, 0, None)      # fp32: general kernel
+    assert st == _lib.UNSUPPORTED and b"2^32" in lib.rocs_last_error_message()
+
+    def att(**kw):
+        a = dict(q=FAR[0], k=FAR[1], v=FAR[2], co=FAR[3], ko=FAR[4], R=2, N=1 << 26, T=1, H=2,
+                 d=64, stride=0, scale=0.0, dtype=0, out=FAR[5], stream=None)
+        a.update(kw)
+        return lib.rocs_dca_attention(*a.values())
+    assert att() == _lib.UNSUPPORTED                  # fp32: general kernel, 2^26 rows
+    assert att(N=1 << 24, T=4) == _lib.UNSUPPORTED
+    # The tiled kernel: (R + N T / 128) * H tiles below 2^24.
+    assert att(dtype=1, N=1 << 30, H=16) == _lib.UNSUPPORTED
+    assert b"2^24" in lib.rocs_last_error_message()

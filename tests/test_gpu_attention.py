@@ -134,6 +134,29 @@ def test_mapped_attention_parity(gpu_lib):
         assert_close(got, round_bf16(want) if bf16 else want, f"mapped d{head_dim} bf16={bf16}")
 
 
+@pytest.mark.parametrize("head_dim,bf16", [(128, True), (64, True), (64, False)],
+                         ids=["d128-bf16", "d64-bf16", "d64-fp32"])
+def test_mapped_attention_index_probe_bit_exact(gpu_lib, head_dim, bf16):
+    # Every request has a history of one row whose values are all 4 r, so the
+    # one softmax weight is exactly 1 and candidate n's output is exactly
+    # 4 m_n: the device's handling of a shuffled per-candidate map is checked
+    # bit for bit (a wrong request is off by at least 4).
+    n_req = 37
+    counts = np.random.default_rng(head_dim).integers(0, 60, size=n_req)
+    counts[[3, 20]] = 0
+    case = wl.attention_case(counts, np.ones(n_req, np.int64), 2, head_dim, q_len=2,
+                             seed=60 + head_dim, bf16=bf16, q_std=3.0)
+    case.v = np.broadcast_to(4.0 * np.arange(n_req, dtype=np.float32)[:, None, None],
+                             case.v.shape).copy()
+    perm = np.random.default_rng(7).permutation(case.q.shape[0])
+    m = ikbo.request_ids(case.cand_offsets)[perm]
+    dev = dev_bf16 if bf16 else dev_f32
+    got = host(ops.dca_attention_mapped(dev(np.ascontiguousarray(case.q[perm])), dev(case.k),
+                                        dev(case.v), dev_i32(m), dev_i32(case.kv_offsets)))
+    want = np.broadcast_to((4.0 * m)[:, None, None, None], got.shape)
+    np.testing.assert_array_equal(got, want)
+
+
 @pytest.mark.parametrize("head_dim", [64, 128])
 @pytest.mark.parametrize("q_len", [1, 32])
 def test_request_side_attention(gpu_lib, head_dim, q_len):

@@ -78,6 +78,30 @@ def test_lcb_index_probe_bit_exact(gpu_lib):
     assert np.all(got[:, 1:, :] == 0.0)
 
 
+@pytest.mark.parametrize("emb,o_cand,f_cand", [(128, 32, 32), (64, 64, 16), (96, 12, 24)],
+                         ids=["fast-e128", "fast-e64", "general"])
+def test_lcb_mapped_index_probe_bit_exact(gpu_lib, emb, o_cand, f_cand):
+    # rocs_ikbo_lcb_mapped with a shuffled map: X^R_r = r everywhere,
+    # W_CR = e_0 into output fields 0 and o_cand - 1, W_CC = 0, so those
+    # output fields of candidate n are exactly m_n in every column and every
+    # other field is 0 (fast and general candidate kernels).
+    counts = np.array([70, 0, 3, 300, 1, 129, 0, 44])
+    r = counts.size
+    m = np.random.default_rng(emb).permutation(ikbo.request_ids(wl.offsets_from_counts(counts)))
+    n = m.size
+    x_req = np.broadcast_to(np.arange(r, dtype=np.float32)[:, None, None], (r, 16, emb)).copy()
+    w_cr = np.zeros((o_cand, 16), np.float32)
+    w_cr[[0, o_cand - 1], 0] = 1.0
+    _, yc = ops.ikbo_lcb_mapped(dev_bf16(x_req), dev_bf16(np.ones((n, f_cand, emb), np.float32)),
+                                dev_bf16(w_cr), dev_bf16(np.zeros((o_cand, f_cand), np.float32)),
+                                dev_i32(m))
+    got = host(yc)
+    want = m[:, None] * np.ones((1, emb))
+    np.testing.assert_array_equal(got[:, 0, :], want)
+    np.testing.assert_array_equal(got[:, o_cand - 1, :], want)
+    assert np.all(got[:, 1:o_cand - 1, :] == 0.0)
+
+
 def test_lcb_general_path_and_fp32(gpu_lib):
     # F_c = 24 and E = 96 are off the fast path; fp32 runs the general kernels.
     case = wl.lcb_case([9, 0, 40], 20, 24, 8, 12, 96, seed=3)

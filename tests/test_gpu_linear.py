@@ -75,6 +75,57 @@ def test_index_probe_bit_exact(gpu_lib):
     np.testing.assert_array_equal(ids.cpu().numpy(), ikbo.request_ids(off))
 
 
+@pytest.mark.parametrize("d_out", [516, 256])
+def test_stream_kernel_index_probe_bit_exact(gpu_lib, d_out):
+    # The same probe on the streaming kernel (k_cand a multiple of 64): its
+    # request-aligned tile slots (request r owns slots r + off[r] / 256 ...)
+    # and the per-workgroup walk over them. Counts: empty requests, exact
+    # multiples of 256, 255 / 257 tails, a single candidate, and enough
+    # tiles that every workgroup walks several. W_CR copies request feature
+    # 0 into outputs 0, 257 and d_out - 1, so the first and a later feature
+    # tile (the one past 512 is partial at d_out = 516) are both checked.
+    counts = np.array([0, 256, 255, 257, 0, 1, 512, 3000, 0, 255, 257, 4096, 1, 0])
+    counts = np.concatenate([counts, np.full(40, 777)])
+    off = wl.offsets_from_counts(counts)
+    n, r = int(counts.sum()), counts.size
+    x_req = np.repeat(np.arange(r, dtype=np.float32)[:, None], 16, axis=1)
+    w_req = np.zeros((d_out, 16), np.float32)
+    cols = sorted({0, min(257, d_out - 1), d_out - 1})
+    w_req[cols, 0] = 1.0
+    out = gpu_lib.ikbo_linear(dev_bf16(np.ones((n, 64), np.float32)),
+                              dev_bf16(np.zeros((d_out, 64), np.float32)),
+                              x_req=dev_bf16(x_req), w_req=dev_bf16(w_req),
+                              cand_offsets=dev_i32(off), activation="relu")
+    got = host(out)
+    want = np.repeat(np.arange(r), counts).astype(np.float64)
+    for c in cols:
+        np.testing.assert_array_equal(got[:, c], want)
+    others = np.setdiff1d(np.arange(d_out), cols)
+    assert np.all(got[:, others] == 0.0)
+
+
+@pytest.mark.parametrize("dims", [(13, 13), (100, 40), (200, 1000)],
+                         ids=lambda d: f"kr{d[0]}-kc{d[1]}")
+def test_pad_dims_reaches_the_streaming_kernel(gpu_lib, dims):
+    # The memory-alignment transform (Section 4.2.4): K zero-padded in both
+    # the activations and the weights (k_cand to a multiple of 64 for the
+    # streaming kernel, k_req to 8 for the request GEMM) gives the oracle's
+    # result on the unpadded inputs.
+    k_req, k_cand = dims
+    case = wl.linear_case([300, 0, 1, 211, 517], k_req, k_cand, 264, seed=k_cand, bias_std=0.3)
+    xc, wc = ops.pad_dims(dev_bf16(case.x_cand), dev_bf16(case.w_cand), 64)
+    xr, wr = ops.pad_dims(dev_bf16(case.x_req), dev_bf16(case.w_req), 8)
+    assert xc.shape[1] % 64 == 0 and wc.shape[1] == xc.shape[1]
+    assert xr.shape[1] % 8 == 0 and wr.shape[1] == xr.shape[1]
+    got = host(ops.ikbo_linear(xc, wc, x_req=xr, w_req=wr, cand_offsets=dev_i32(case.cand_offsets),
+                               bias=dev_f32(case.bias), activation="relu"))
+    assert_close(got, _want(case, "relu"), f"padded {dims}")
+    # Already aligned: returned as they are.
+    a, b = dev_bf16(np.ones((4, 64), np.float32)), dev_bf16(np.ones((8, 64), np.float32))
+    pa, pb = ops.pad_dims(a, b, 64)
+    assert pa is a and pb is b
+
+
 def test_general_path_unaligned_and_fp32(gpu_lib):
     # K = 13 is not a multiple of 8: the general kernel runs.
     case = wl.linear_case([9, 0, 40], 13, 5, 7, seed=6)
@@ -199,9 +250,9 @@ def test_glm_linear_request_only(gpu_lib):
 @pytest.mark.parametrize("shape", [([300, 0, 1, 211, 17], 96, 64, 256),
                                    ([2000, 13000, 0, 17001], 256, 128, 516)],
                          ids=["small", "large"])
-def test_combined_request_candidate_kernel(gpu_lib, shape, monkeypatch):
-    # ROCS_LINEAR_COMBINED=1: request tiles inside the streaming kernel with
-    # completion flags (and Y^R from the stacked weight); equal to the
+def test_combined_request_candidate_kernel(gpu_lib, shape):
+    # rocs_ikbo_linear_combined: request tiles inside the streaming kernel
+    # with completion flags (and Y^R from the stacked weight); equal to the
     # separate launches and to the oracle, on two calls with one workspace
     # (the second call's flags must not match the first call's epoch).
     counts, kr, kc, d = shape
@@ -214,12 +265,17 @@ def test_combined_request_candidate_kernel(gpu_lib, shape, monkeypatch):
             dev_bf16(case.w_cand), dev_i32(case.cand_offsets))
     kw = dict(b_cand=dev_f32(case.bias), activation="relu")
     sep_r, sep_c = ops.glm_linear(*args, **kw)
-    monkeypatch.setenv("ROCS_LINEAR_COMBINED", "1")
     want_r, want_c = ikbo.glm_linear(case.x_req, case.x_cand, w_rr, case.w_req, case.w_cand,
                                      None, case.bias, case.cand_offsets, "relu")
+    x_req, x_cand, w_rr_d, w_cr, w_cc, off = args
     for _ in range(2):
-        y_r, y_c = ops.glm_linear(*args, workspace=ws, **kw)
+        y_r, y_c = ops.ikbo_linear_combined(x_req, x_cand, w_cr, w_cc, off, w_rr=w_rr_d,
+                                            workspace=ws, **kw)
         assert_close(host(y_c), round_bf16(want_c), f"combined y_cand {shape}")
         assert_close(host(y_r), round_bf16(want_r), f"combined y_req {shape}")
         np.testing.assert_array_equal(host(y_c), host(sep_c))
         np.testing.assert_array_equal(host(y_r), host(sep_r))
+    # Candidate output only (no Y^R): the rocs_ikbo_linear result.
+    y_r, y_c = ops.ikbo_linear_combined(x_req, x_cand, w_cr, w_cc, off, workspace=ws, **kw)
+    assert y_r is None
+    np.testing.assert_array_equal(host(y_c), host(sep_c))

@@ -1,35 +1,27 @@
 """GPU parity on the five benchmark workloads at their full sizes, in the
 launch configuration the benchmark times.
 
-Outputs are compared with the oracle pipelines on sampled candidates (every
-request's first and last candidate, tile boundaries and random rows, over a
-subset of requests where the request-side oracle work is large); request-side
-outputs are compared in full. Both sides round to bf16 at the same operator
-boundaries.
+Candidate-side outputs are compared with the oracle pipelines on one random
+row from every 128-row block of every request (blocks start at the request's
+first candidate, as the attention and IKBO GEMM tiles do), plus each
+request's first and last candidate. Every 128-row attention tile and every
+request-aligned 256-row GEMM tile thus has a compared row. So does every
+256-row tile of the plain GEMMs, whose tiles run over the candidate rows
+contiguously: any 256 consecutive rows contain a whole block of at most 128
+rows. Request-side outputs are compared in full. Both sides round to bf16 at
+the same operator boundaries; properties that hold at any size (finite
+outputs, ReLU outputs non-negative) are checked on every candidate.
 """
 
 import numpy as np
 import pytest
 import torch
 
-from gpu_util import assert_close, host
+from gpu_util import assert_close, host, tile_rows
 from oracle import pipelines as oracle_pipelines
 from paper_2607_27744_amd import pipelines, workloads as wl
 
 pytestmark = pytest.mark.gpu
-
-
-def _sample_rows(off, requests, per_request, seed):
-    rng = np.random.default_rng(seed)
-    rows = []
-    for r in requests:
-        a, b = int(off[r]), int(off[r + 1])
-        if b == a:
-            continue
-        pick = {a, b - 1, min(a + 255, b - 1), min(a + 256, b - 1)}
-        pick.update(rng.integers(a, b, size=per_request).tolist())
-        rows.extend(sorted(pick))
-    return np.array(sorted(set(rows)), dtype=np.int64)
 
 
 def _say(msg):
@@ -42,7 +34,7 @@ def _gpu(w):
     p = pipelines.prepare(w)
     pipelines.step(p)
     torch.cuda.synchronize()
-    _say("GPU done; oracle on sampled candidates")
+    _say("GPU done; oracle on one row of every tile")
     return pipelines.outputs(p)
 
 
@@ -61,42 +53,54 @@ def test_workload1_tiny_block_fp32(gpu_lib):
 
 
 def test_workload2_retrieval_mlp(gpu_lib):
+    # Both layers in one kernel (the hidden layer on chip): the output is
+    # compared with the oracle's composition, H rounded to bf16 between layers.
     w = wl.make_workload(2)
     got = _gpu(w)
-    rows = _sample_rows(w.cand_offsets, range(w.n_req), 24, 2)
+    rows = tile_rows(w.cand_offsets, 2)
     want = oracle_pipelines.retrieval_mlp(w, rows=rows)
-    assert_close(_rows(got["h1"], rows), want["h1"], "h1")
+    _say(f"{rows.size} rows compared")
     assert_close(_rows(got["out"], rows), want["out"], "out")
+    assert bool(torch.isfinite(got["out"]).all())
 
 
 def test_workload3_ranking_dca(gpu_lib):
     w = wl.make_workload(3)
     got = _gpu(w)
-    reqs = [0, 1, 77, 128, 200, 254, 255]
-    rows = _sample_rows(w.cand_offsets, reqs, 16, 3)
+    rows = tile_rows(w.cand_offsets, 3)
     want = oracle_pipelines.ranking_dca(w, rows=rows)
+    _say(f"{rows.size} rows compared")
     for key in ("q1", "a1", "q2", "a2"):
         assert_close(_rows(got[key], rows), want[key], key)
+        assert bool(torch.isfinite(got[key]).all())
 
 
 def test_workload4_fm_linear(gpu_lib):
+    # The interaction fused into the linear's operand: Y^R (request side, in
+    # full) and the output are compared.
     w = wl.make_workload(4)
     got = _gpu(w)
-    rows = _sample_rows(w.cand_offsets, range(0, w.n_req, 9), 12, 4)
+    rows = tile_rows(w.cand_offsets, 4)
     want = oracle_pipelines.fm_linear(w, rows=rows)
+    _say(f"{rows.size} rows compared")
     assert_close(host(got["y_req"]), want["y_req"], "y_req")
-    assert_close(_rows(got["y_cand"], rows), want["y_cand"], "y_cand")
     assert_close(_rows(got["out"], rows), want["out"], "out")
+    assert bool((got["out"] >= 0).all())
 
 
-@pytest.mark.timeout(600)
+@pytest.mark.timeout(900)
 def test_workload5_production_retrieval(gpu_lib):
     w = wl.make_workload(5)
     got = _gpu(w)
-    rows = _sample_rows(w.cand_offsets, [0, 5, 10, 15], 16, 5)
-    want = oracle_pipelines.production_retrieval(w, rows=rows)
-    for key in ("h1", "out2", "attention"):
-        assert_close(_rows(got[key], rows), want[key], key)
+    rows = tile_rows(w.cand_offsets, 5)
+    _say(f"oracle on {rows.size} rows of all {w.n_req} requests, four requests at a time")
+    off = np.asarray(w.cand_offsets, dtype=np.int64)
+    for r0 in range(0, w.n_req, 4):
+        part = rows[(rows >= off[r0]) & (rows < off[min(r0 + 4, w.n_req)])]
+        want = oracle_pipelines.production_retrieval(w, rows=part)
+        for key in ("h1", "out2", "attention"):
+            assert_close(_rows(got[key], part), want[key], f"{key} requests {r0}..{r0 + 3}")
+        _say(f"requests {r0}..{r0 + 3}: {part.size} rows match")
     # Properties that hold at any size, checked on every candidate.
     assert bool(torch.isfinite(got["attention"]).all()) and bool(torch.isfinite(got["out2"]).all())
     assert bool((got["h1"] >= 0).all())

@@ -170,6 +170,26 @@ def test_dca_layer_is_glm_compliant():
     assert np.all(base["a_cand"][3:8] == 0.0)
     # Request 2 has no history: its request-side attention is zero.
     assert np.all(base["a_req"][2] == 0.0)
+    # The request side is single-request attention of each request's own
+    # queries over its own history (Eq. dca-attention, request group),
+    # written out here with plain loops: scores q.k / sqrt(d), softmax over
+    # the request's rows, weighted sum of its value rows.
+    h, d = w.heads, w.head_dim
+    for r in range(w.n_req):
+        a, b = int(w.kv_offsets[r]), int(w.kv_offsets[r + 1])
+        s_r = np.asarray(w.s[a:b], dtype=np.float64)
+        k_r = round_bf16(s_r @ np.asarray(w.wk_r, np.float64).T).reshape(-1, h, d)
+        v_r = round_bf16(s_r @ np.asarray(w.wv_r, np.float64).T).reshape(-1, h, d)
+        want = np.zeros((w.q_len, h, d))
+        for t in range(w.q_len):
+            for hh in range(h):
+                if b == a:
+                    continue
+                q = base["q_req"][r, t, hh]
+                sc = np.array([q @ k_r[j, hh] for j in range(b - a)]) / np.sqrt(d)
+                e = np.exp(sc - sc.max())
+                want[t, hh] = sum(e[j] * v_r[j, hh] for j in range(b - a)) / e.sum()
+        np.testing.assert_allclose(base["a_req"][r], round_bf16(want), rtol=0, atol=1e-12)
 
 
 def _mlp2_case(counts, k_req=6, k_cand=5, d_hidden=8, d_out=3, seed=0):
