@@ -190,6 +190,38 @@ int32_t rocs_ikbo_linear_combined(const void* x_req, int64_t k_req,
 
 /*
  * ---------------------------------------------------------------------------
+ * rocs_ikbo_linear_noalloc: rocs_ikbo_linear for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation). It takes no workspace: the request table Z and the
+ * index map live in a static scratch array of ROCS_NOALLOC_SCRATCH_BYTES
+ * that the library holds on each device it runs on until the process ends.
+ * The call itself allocates and frees nothing; the first call on a device
+ * looks up that device's copy of the array (once).
+ *
+ *   Arguments, result, fast path and errors as for rocs_ikbo_linear, without
+ *   workspace / workspace_bytes. The call needs
+ *   rocs_ikbo_linear_workspace_size(R, N, d_out, k_req) <=
+ *   ROCS_NOALLOC_SCRATCH_BYTES (for example R = 16, d_out = 1024 and up to
+ *   about four million candidates); a larger call returns
+ *   ROCS_ERR_WORKSPACE_TOO_SMALL before touching the device.
+ *
+ * All calls on one device share its scratch array, and a call leaves its own
+ * contents there (nothing in it needs clearing: every call writes what it
+ * reads). Calls that overlap in time on one device (concurrent streams,
+ * threads) race on it and must be serialised by the caller.
+ * ---------------------------------------------------------------------------
+ */
+#define ROCS_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+int32_t rocs_ikbo_linear_noalloc(const void* x_req, int64_t k_req,
+                                 const void* x_cand, const void* x_cand_add, int64_t k_cand,
+                                 const void* w_req, const void* w_cand, const float* bias,
+                                 const int32_t* cand_offsets,
+                                 int64_t num_requests, int64_t num_cand, int64_t d_out,
+                                 int32_t dtype, int32_t activation, void* out, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * rocs_ikbo_linear_mapped: rocs_ikbo_linear with the index map m given as a
  * per-candidate request id instead of CSR offsets (Section 4.1 defines m as
  * any map {0..B_c-1} -> {0..B_r-1}; candidates of one request need not be

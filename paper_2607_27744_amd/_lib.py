@@ -26,6 +26,8 @@ SIGNATURES = {
     "rocs_ikbo_linear_combined": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _vp,
                                          _vp, _i64, _i64, _i64, _i64, _i32, _i32, _vp, _vp, _vp,
                                          _size, _vp]),
+    "rocs_ikbo_linear_noalloc": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
+                                        _i64, _i64, _i64, _i32, _i32, _vp, _vp]),
     "rocs_ikbo_linear_mapped": (_i32, [_vp, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
                                        _i64, _i64, _i64, _i32, _i32, _vp, _vp, _size, _vp]),
     "rocs_dca_attention": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32,
@@ -50,6 +52,7 @@ SIGNATURES = {
 }
 
 ABI_VERSION = 1
+NOALLOC_SCRATCH_BYTES = 16 << 20   # ROCS_NOALLOC_SCRATCH_BYTES
 
 
 class RocsError(RuntimeError):

@@ -5,6 +5,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -261,6 +262,72 @@ int32_t rocs_ikbo_linear_combined(const void* x_req, int64_t k_req, const void* 
   return linear_impl("rocs_ikbo_linear_combined", false, x_req, k_req, x_cand, x_cand_add,
                      k_cand, w_cr, w_cc, b_cand, cand_offsets, nullptr, R, N, d_cand, dtype,
                      activation, y_cand, workspace, workspace_bytes, stream, rs, true);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of rocs_ikbo_linear_noalloc: the request table Z and the index map
+// live in this array instead of a caller's workspace. Each device that runs
+// the library holds its own copy until the process ends. In host code the
+// name only stands in for the symbol; the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kScratchBytes = ROCS_NOALLOC_SCRATCH_BYTES;
+static __device__ __attribute__((aligned(256))) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchSlot {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// The current device's copy of `scratch` (its device address).
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  ScratchSlot& slot = g_scratch[dev];
+  std::call_once(slot.once, [&slot] {
+    slot.err = hipGetSymbolAddress(&slot.ptr, HIP_SYMBOL(scratch));
+  });
+  if (slot.err != hipSuccess) return slot.err;
+  *out = slot.ptr;
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rocs_ikbo_linear_noalloc(const void* x_req, int64_t k_req, const void* x_cand,
+                                 const void* x_cand_add, int64_t k_cand, const void* w_req,
+                                 const void* w_cand, const float* bias,
+                                 const int32_t* cand_offsets, int64_t R, int64_t N,
+                                 int64_t d_out, int32_t dtype, int32_t activation, void* out,
+                                 void* stream) {
+  // Size first, before any HIP call: the request table and the index map
+  // must fit the static scratch array.
+  const size_t need = rocs_ikbo_linear_workspace_size(R, N, d_out, k_req);
+  if (need > kScratchBytes)
+    return fail(ROCS_ERR_WORKSPACE_TOO_SMALL,
+                "rocs_ikbo_linear_noalloc: needs %zu bytes of scratch for R=%lld N=%lld "
+                "d_out=%lld; the library's static scratch holds %zu (use rocs_ikbo_linear "
+                "with a workspace)", need, (long long)R, (long long)N, (long long)d_out,
+                kScratchBytes);
+  void* ws = nullptr;
+  if (need > 0 && N > 0) {
+    const hipError_t e = scratch_address(&ws);
+    if (e != hipSuccess)
+      return fail(ROCS_ERR_HIP, "rocs_ikbo_linear_noalloc: scratch address: %s",
+                  hipGetErrorString(e));
+  }
+  return linear_impl("rocs_ikbo_linear_noalloc", false, x_req, k_req, x_cand, x_cand_add,
+                     k_cand, w_req, w_cand, bias, cand_offsets, nullptr, R, N, d_out, dtype,
+                     activation, out, ws, ws != nullptr ? kScratchBytes : 0, stream);
 }
 
 int32_t rocs_ikbo_linear_mapped(const void* x_req, int64_t k_req, const void* x_cand,
