@@ -236,11 +236,17 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   // exceeds it by more than 2^kLazyRescale (always on the first stage).
   auto row_max = [&](f32x16 (&sacc)[KB], auto masked, int valid) {
     if constexpr (decltype(masked)::value) {
+      // One 16-key group at a time: issued all at once, the 32 compares would
+      // hold 32 lane masks (64 scalar registers) and push values to scratch.
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-          if (32 * kb + 8 * (e / 4) + 4 * hh + (e % 4) >= valid) sacc[kb][e] = -INFINITY;
+        for (int qq = 0; qq < 4; ++qq) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (32 * kb + 8 * qq + 4 * hh + i >= valid) sacc[kb][4 * qq + i] = -INFINITY;
+          __builtin_amdgcn_sched_barrier(0);
+        }
     }
     // Row max: 32 keys per lane, then across the two wave halves.
     float mx = sacc[0][0];
@@ -382,10 +388,12 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   }
   if (kt + 1 < ntiles) {
     step(kt, s_a, s_b);
-    if (active) last_stage((ntiles - 1) % kStages, s_b);
-  } else if (active) {
-    last_stage((ntiles - 1) % kStages, s_a);
+    if (active) {                              // one call site for the last stage
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) s_a[kb] = s_b[kb];
+    }
   }
+  if (active) last_stage((ntiles - 1) % kStages, s_a);
 
   // Epilogue through LDS. Once every wave is past its last stage the K/V
   // ring is idle; each wave writes its 32 normalised output rows there
@@ -394,6 +402,12 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   // 2D-byte row segments instead of 16 bytes of 32 different rows.
   ring_barrier();
   if (!active) return;
+  // The epilogue's addresses come from a laundered copy of the lane index:
+  // derived from `lane` directly, the compiler computes them at the start
+  // and holds them through the main loop, where the registers are short.
+  int lane_e = lane;
+  asm volatile("" : "+v"(lane_e));
+  const int l32e = lane_e & 31, hhe = lane_e >> 5;
   // Element 4 qq + i of oacc[db] is O[row l32][dim 32 db + 8 qq + 4 hh + i];
   // after the swap lane (l32, hh) holds dims 32 db + 16 j + 8 hh .. +7
   // (16-byte chunk 4 db + 2 j + hh of the row).
@@ -411,18 +425,18 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
       const uint32_t o1 = pack_bf16x2(o[8 * j + 6] * inv, o[8 * j + 7] * inv);
       const auto s0 = __builtin_amdgcn_permlane32_swap(e0, o0, false, false);
       const auto s1 = __builtin_amdgcn_permlane32_swap(e1, o1, false, false);
-      const int chunk = (4 * db + 2 * j + hh) ^ out_swz(l32);
-      *reinterpret_cast<ROCS_LDS u32x4*>(lds3 + obase + l32 * ROWB + 16 * chunk) =
+      const int chunk = (4 * db + 2 * j + hhe) ^ out_swz(l32e);
+      *reinterpret_cast<ROCS_LDS u32x4*>(lds3 + obase + l32e * ROWB + 16 * chunk) =
           u32x4{s0[0], s1[0], s0[1], s1[1]};
     }
   constexpr int RPS = 1024 / ROWB;            // output rows per store instruction
 #pragma unroll
   for (int i = 0; i < 32 / RPS; ++i) {
-    const int row = RPS * i + lane / CR;
+    const int row = RPS * i + lane_e / CR;
     const u32x4 v = *reinterpret_cast<const ROCS_LDS u32x4*>(
-        lds3 + obase + row * ROWB + 16 * ((lane % CR) ^ out_swz(row)));
+        lds3 + obase + row * ROWB + 16 * ((lane_e % CR) ^ out_swz(row)));
     if (wrow0 + row < rows)
-      *reinterpret_cast<u32x4*>(oh + (int64_t)(wrow0 + row) * qs + 8 * (lane % CR)) = v;
+      *reinterpret_cast<u32x4*>(oh + (int64_t)(wrow0 + row) * qs + 8 * (lane_e % CR)) = v;
   }
 }
 
