@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define ROCS_ABI_VERSION 1
+#define ROCS_ABI_VERSION 2
 
 typedef enum rocs_status {
   ROCS_OK = 0,
@@ -301,19 +301,38 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
  *   cand_request_ids [N] int32, device memory, each in [0, R) (trusted; an
  *                    id outside the range is clamped into it, so it gives
  *                    wrong rows, never an access outside kv_offsets).
+ *   workspace        device memory of at least
+ *                    rocs_dca_attention_mapped_workspace_size(R, N) bytes,
+ *                    256-byte aligned (may be NULL when that size is 0 or the
+ *                    general kernel runs). Contents on entry are ignored. On
+ *                    return, when the tiled kernel ran, it holds the grouping
+ *                    described below at offset 0: grp_off [R + 1] int32, then,
+ *                    at the next 256-byte boundary, order [N] int32.
  * Every other argument, the result and the errors are those of
- * rocs_dca_attention. Request tiles need contiguous candidates, so this
- * entry point runs the general kernel (one wave per query row and head,
- * history read through L2); reorder candidates by request and use
- * rocs_dca_attention for throughput.
+ * rocs_dca_attention.
+ *
+ * IKBO form on the fast path (the conditions of rocs_dca_attention): the
+ * candidates are first grouped by request on the device, a stable counting
+ * sort: order[p] lists request 0's candidates, then request 1's, ..., each
+ * request's in their original order, and grp_off are the CSR offsets of that
+ * order. The tiled kernel then runs on the grouped order, gathering query
+ * rows and scattering output rows through `order`, so each request's K/V
+ * is read once per tile of its candidates. This needs R <= 16384 and
+ * R * ceil(N / G) <= 2^20 for a block size G of at least 4096 (the
+ * workspace size is 0 otherwise). Other calls run the general kernel (one
+ * wave per query row and head, history read through L2), which needs no
+ * workspace.
  * ---------------------------------------------------------------------------
  */
+size_t rocs_dca_attention_mapped_workspace_size(int64_t num_requests, int64_t num_cand);
+
 int32_t rocs_dca_attention_mapped(const void* q, const void* k, const void* v,
                                   const int32_t* cand_request_ids, const int32_t* kv_offsets,
                                   int64_t num_requests, int64_t num_cand,
                                   int32_t q_len, int32_t num_heads, int32_t head_dim,
                                   int64_t kv_row_stride, float softmax_scale, int32_t dtype,
-                                  void* out, void* stream);
+                                  void* out, void* workspace, size_t workspace_bytes,
+                                  void* stream);
 
 /*
  * ---------------------------------------------------------------------------

@@ -32,8 +32,9 @@ SIGNATURES = {
                                        _i64, _i64, _i64, _i32, _i32, _vp, _vp, _size, _vp]),
     "rocs_dca_attention": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32,
                                   _i64, _f32, _i32, _vp, _vp]),
+    "rocs_dca_attention_mapped_workspace_size": (_size, [_i64, _i64]),
     "rocs_dca_attention_mapped": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32,
-                                         _i64, _f32, _i32, _vp, _vp]),
+                                         _i64, _f32, _i32, _vp, _vp, _size, _vp]),
     "rocs_glm_interaction": (_i32, [_vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32, _i32,
                                     _vp, _vp, _vp]),
     "rocs_ikbo_lcb_workspace_size": (_size, [_i64, _i64, _i64]),
@@ -51,7 +52,7 @@ SIGNATURES = {
     "rocs_validate_offsets": (_i32, [_vp, _i64, _i64, _vp]),
 }
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 NOALLOC_SCRATCH_BYTES = 16 << 20   # ROCS_NOALLOC_SCRATCH_BYTES
 
 

@@ -351,7 +351,8 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
                        const void* v, const int32_t* cand_offsets, const int32_t* cand_ids,
                        const int32_t* kv_offsets, int64_t R, int64_t N, int32_t q_len,
                        int32_t num_heads, int32_t head_dim, int64_t kv_row_stride,
-                       float softmax_scale, int32_t dtype, void* out, void* stream) {
+                       float softmax_scale, int32_t dtype, void* out, void* stream,
+                       void* workspace = nullptr, size_t workspace_bytes = 0) {
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (R < 0 || N < 0 || q_len < 1 || num_heads < 1 || head_dim < 1 || kv_row_stride < 0)
     return fail(ROCS_ERR_INVALID_ARGUMENT,
@@ -392,14 +393,32 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
                     aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16);
   // Launch limits: a grid may hold fewer than 2^32 work items. The general
   // kernel runs one 64-lane wave per (query row, head) with the rows on the
-  // grid's x axis; the tiled kernel (CSR only) runs 256 lanes per (head,
-  // tile slot), R + ceil(N q_len / 128) slots per head.
-  if ((!fast || mapped) && (N * q_len) >= (int64_t(1) << 26))
+  // grid's x axis; the tiled kernel runs 256 lanes per (head, tile slot),
+  // R + ceil(N q_len / 128) slots per head.
+  // The mapped form runs the tiled kernel on the candidates grouped by
+  // request when the grouping fits (R and the per-block count table), with
+  // the grouping in the caller's workspace; otherwise the general kernel.
+  const size_t group_bytes = mapped ? rocs::mapped_grouping_bytes(R, N) : 0;
+  const bool tiled = fast && (!mapped || group_bytes > 0);
+  if (mapped && tiled) {
+    if (workspace == nullptr || workspace_bytes < group_bytes)
+      return fail(ROCS_ERR_WORKSPACE_TOO_SMALL, "%s: workspace needs %zu bytes, got %zu", name,
+                  group_bytes, workspace == nullptr ? (size_t)0 : workspace_bytes);
+    if (!aligned(workspace, 256))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: workspace must be 256-byte aligned", name);
+    if (overlap(workspace, group_bytes, out, out_bytes) ||
+        overlap(workspace, group_bytes, q, out_bytes) ||
+        overlap(workspace, group_bytes, cand_ids, (size_t)N * 4) ||
+        overlap(workspace, group_bytes, kv_offsets, (size_t)(R + 1) * 4))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: workspace overlaps an argument", name);
+  }
+  if (!tiled && (N * q_len) >= (int64_t(1) << 26))
     return fail(ROCS_ERR_UNSUPPORTED, "%s: N * q_len = %lld query rows exceed the general "
                 "kernel's grid (2^26 rows)", name, (long long)(N * q_len));
-  if (fast && !mapped && (R + (N * q_len + 127) / 128) * num_heads >= (int64_t(1) << 24))
+  if (tiled && (R + (N * q_len + 127) / 128) * num_heads >= (int64_t(1) << 24))
     return fail(ROCS_ERR_UNSUPPORTED, "%s: (R + N * q_len / 128) * num_heads tiles exceed the "
                 "grid limit (2^24)", name);
+  a.workspace = mapped && tiled ? workspace : nullptr;
   const hipError_t e = rocs::launch_attention(a, fast, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return launch_failed(name, e);
   return ok();
@@ -419,14 +438,20 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
                         softmax_scale, dtype, out, stream);
 }
 
+size_t rocs_dca_attention_mapped_workspace_size(int64_t num_requests, int64_t num_cand) {
+  if (num_requests <= 0 || num_cand <= 0) return 0;
+  return rocs::mapped_grouping_bytes(num_requests, num_cand);
+}
+
 int32_t rocs_dca_attention_mapped(const void* q, const void* k, const void* v,
                                   const int32_t* cand_request_ids, const int32_t* kv_offsets,
                                   int64_t R, int64_t N, int32_t q_len, int32_t num_heads,
                                   int32_t head_dim, int64_t kv_row_stride, float softmax_scale,
-                                  int32_t dtype, void* out, void* stream) {
+                                  int32_t dtype, void* out, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
   return attention_impl("rocs_dca_attention_mapped", true, q, k, v, nullptr, cand_request_ids,
                         kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
-                        softmax_scale, dtype, out, stream);
+                        softmax_scale, dtype, out, stream, workspace, workspace_bytes);
 }
 
 int32_t rocs_glm_interaction(const void* x_req, const void* x_cand, const int32_t* cand_offsets,

@@ -27,6 +27,10 @@ namespace rocs {
 namespace {
 
 constexpr int kTileKeys = 64;    // history rows per K/V stage
+constexpr int kGroupMaxRequests = 16384;            // LDS counters of the grouping kernels
+constexpr int64_t kGroupMaxHist = int64_t(1) << 20;  // per-block counts scanned by one workgroup
+
+size_t align_up256(size_t n) { return (n + 255) & ~size_t(255); }
 // Online softmax bound. A stage's weights, taken against the running max as
 // it stands, are accepted as they are while their per-lane sum is at most
 // 2^64. Otherwise the stage takes its row max, and the running max moves to
@@ -88,12 +92,17 @@ template <int D> constexpr int attn_waves() { return 4; }  // query rows / 32 pe
 // on ranking-sized histories.)
 constexpr int kRingSlots = 2;
 
-template <int D, int W>
+// MAPPED: the candidates arrive grouped by request through a permutation
+// (Section 4.3.1 with a general map m): cand_off are the offsets of the
+// grouped order and grouped position p holds candidate order[p], so query
+// rows are gathered and output rows scattered through `order`; everything
+// else is the CSR kernel.
+template <int D, int W, bool MAPPED>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void dca_attn_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
-    int64_t slots_per_head) {
+    int64_t slots_per_head, const int32_t* __restrict__ order) {
   constexpr int NT = 64 * W;
   constexpr int TR = 32 * W;           // query rows per tile
   constexpr int KB = kTileKeys / 32;   // 32-key blocks per stage
@@ -127,13 +136,25 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   const int64_t kv0 = kv_off[r];
   const int L = kv_off[r + 1] - (int)kv0;
   const int64_t qs = (int64_t)H * D;                      // q / out row stride
-  const bf16_t* qh = q + row0 * qs + (int64_t)h * D;
-  bf16_t* oh = out + row0 * qs + (int64_t)h * D;
+  // Query / output row of the tile's row i (i < rows): row0 + i directly,
+  // or through the grouped order (grouped candidate p = row / T_q holds
+  // candidate order[p]).
+  auto src_row = [&](int i) -> int64_t {
+    const int64_t gr = row0 + i;
+    if constexpr (MAPPED) {
+      const int64_t p = gr / Tq;
+      return (int64_t)order[p] * Tq + (gr - p * Tq);
+    } else {
+      return gr;
+    }
+  };
+  const bf16_t* qh = q + (int64_t)h * D;
+  bf16_t* oh = out + (int64_t)h * D;
 
   if (L == 0) {                                           // empty history: zeros
     for (int c = tid; c < rows * (D / 8); c += NT) {
       const int rr = c / (D / 8), dc = (c % (D / 8)) * 8;
-      *reinterpret_cast<u32x4*>(oh + rr * qs + dc) = u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(oh + src_row(rr) * qs + dc) = u32x4{0u, 0u, 0u, 0u};
     }
     return;
   }
@@ -145,7 +166,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   bf16x8 qf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
-    qf[ks] = *reinterpret_cast<const bf16x8*>(qh + qrow * qs + 16 * ks + 8 * hh);
+    qf[ks] = *reinterpret_cast<const bf16x8*>(qh + src_row(qrow) * qs + 16 * ks + 8 * hh);
 
   // DMA staging. Load i of wave w fills LDS rows KPI (NI w + i) .. +KPI-1 of
   // the stage, 16 bytes per lane in lane order: lane -> row KPI (NI w + i) +
@@ -436,7 +457,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
     const u32x4 v = *reinterpret_cast<const ROCS_LDS u32x4*>(
         lds3 + obase + row * ROWB + 16 * ((lane_e % CR) ^ out_swz(row)));
     if (wrow0 + row < rows)
-      *reinterpret_cast<u32x4*>(oh + (int64_t)(wrow0 + row) * qs + 8 * (lane_e % CR)) = v;
+      *reinterpret_cast<u32x4*>(oh + src_row(wrow0 + row) * qs + 8 * (lane_e % CR)) = v;
   }
 }
 
@@ -498,18 +519,133 @@ __global__ __launch_bounds__(64) void dca_attn_generic(
   }
 }
 
-template <int D>
-hipError_t launch_fast(const AttentionArgs& a, hipStream_t s) {
+// ---------------------------------------------------------------------------
+// Grouping a per-candidate request map by request, a stable counting sort,
+// so that the tiled kernel also serves a general map (Section 4.3.1: resolve
+// m_i, then share the request's K/V). order[p] lists request 0's candidates
+// first, then request 1's, ..., each request's candidates in their original
+// order; grp_off[R + 1] are the CSR offsets of that order. The candidates
+// are cut into nb blocks of G; hist[r * nb + b] counts request r in block b,
+// and its exclusive scan in that (request-major) order is the grouped
+// position of request r's first candidate in block b. Ids outside [0, R)
+// are clamped into range, as the other kernels do.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int clamp_request(int32_t m, int R) {
+  return (int)min((uint32_t)m, (uint32_t)(R - 1));
+}
+
+__global__ __launch_bounds__(256) void group_count(const int32_t* __restrict__ ids, int64_t N,
+                                                   int R, int64_t G, int nb,
+                                                   int32_t* __restrict__ hist) {
+  __shared__ int cnt[kGroupMaxRequests];
+  const int b = blockIdx.x;
+  for (int r = threadIdx.x; r < R; r += 256) cnt[r] = 0;
+  __syncthreads();
+  const int64_t lo = (int64_t)b * G, hi = min(lo + G, N);
+  for (int64_t i = lo + threadIdx.x; i < hi; i += 256) atomicAdd(&cnt[clamp_request(ids[i], R)], 1);
+  __syncthreads();
+  for (int r = threadIdx.x; r < R; r += 256) hist[(int64_t)r * nb + b] = cnt[r];
+}
+
+// One workgroup: exclusive scan of hist[0 .. total) in place (each thread
+// owns a contiguous run; the run sums are scanned in LDS), then the grouped
+// offsets grp_off[r] = scan[r * nb], grp_off[R] = N.
+__global__ __launch_bounds__(1024) void group_scan(int32_t* __restrict__ hist, int64_t total,
+                                                   int R, int nb, int64_t N,
+                                                   int32_t* __restrict__ grp_off) {
+  __shared__ int part[1024];
+  const int t = threadIdx.x;
+  const int64_t per = (total + 1023) / 1024;
+  const int64_t lo = min((int64_t)t * per, total), hi = min(lo + per, total);
+  int sum = 0;
+  for (int64_t i = lo; i < hi; ++i) sum += hist[i];
+  part[t] = sum;
+  __syncthreads();
+  for (int d = 1; d < 1024; d <<= 1) {                    // inclusive scan of the run sums
+    const int add = t >= d ? part[t - d] : 0;
+    __syncthreads();
+    part[t] += add;
+    __syncthreads();
+  }
+  int acc = part[t] - sum;                                // exclusive
+  for (int64_t i = lo; i < hi; ++i) {
+    const int c = hist[i];
+    hist[i] = acc;
+    acc += c;
+  }
+  __threadfence_block();
+  __syncthreads();
+  for (int r = t; r < R; r += 1024) grp_off[r] = hist[(int64_t)r * nb];
+  if (t == 0) grp_off[R] = (int)N;
+}
+
+// One wave per block, walking its candidates in order 64 at a time: lanes
+// holding the same request take consecutive slots from that request's
+// cursor in lane order (ballot ranks), so the order within a request is
+// the original one.
+__global__ __launch_bounds__(64) void group_scatter(const int32_t* __restrict__ ids, int64_t N,
+                                                    int R, int64_t G, int nb,
+                                                    const int32_t* __restrict__ base,
+                                                    int32_t* __restrict__ order) {
+  __shared__ int cursor[kGroupMaxRequests];
+  const int b = blockIdx.x, lane = threadIdx.x;
+  for (int r = lane; r < R; r += 64) cursor[r] = base[(int64_t)r * nb + b];
+  __syncthreads();
+  const int64_t lo = (int64_t)b * G, hi = min(lo + G, N);
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int64_t c = lo; c < hi; c += 64) {
+    const int64_t i = c + lane;
+    const bool valid = i < hi;
+    const int key = valid ? clamp_request(ids[i], R) : -1;
+    uint64_t todo = __ballot(valid);
+    while (todo != 0) {
+      const int leader = __builtin_ctzll(todo);
+      const int k0 = __shfl(key, leader);
+      const uint64_t same = __ballot(valid && key == k0);
+      const int at = cursor[k0];                          // read by every lane first ...
+      if (valid && key == k0) order[at + __builtin_popcountll(same & below)] = (int)i;
+      if (lane == leader) cursor[k0] = at + __builtin_popcountll(same);   // ... then advanced
+      todo &= ~same;
+    }
+  }
+}
+
+template <int D, bool MAPPED>
+hipError_t launch_fast(const AttentionArgs& a, const int32_t* cand_off, const int32_t* order,
+                       hipStream_t s) {
   constexpr int W = attn_waves<D>(), TR = 32 * W;
   const int64_t slots = a.R + (a.N * a.q_len + TR - 1) / TR;
   const int64_t grid = slots * a.heads;
   const float scale_log2 = a.scale * 1.4426950408889634f;
   if (!grid_fits(grid, 64 * W)) return hipErrorInvalidConfiguration;
-  return launch_kernel(dca_attn_bf16<D, W>, dim3((uint32_t)grid), dim3(64 * W), s,
+  return launch_kernel(dca_attn_bf16<D, W, MAPPED>, dim3((uint32_t)grid), dim3(64 * W), s,
                        static_cast<const bf16_t*>(a.q), static_cast<const bf16_t*>(a.k),
-                       static_cast<const bf16_t*>(a.v), a.cand_offsets, a.kv_offsets,
+                       static_cast<const bf16_t*>(a.v), cand_off, a.kv_offsets,
                        static_cast<bf16_t*>(a.out), (int)a.R, a.q_len, a.heads, a.kv_stride,
-                       scale_log2, slots);
+                       scale_log2, slots, order);
+}
+
+// The mapped form on the tiled kernel: group, then attend in grouped order.
+template <int D>
+hipError_t launch_fast_mapped(const AttentionArgs& a, hipStream_t s) {
+  int64_t G = 0;
+  int nb = 0;
+  if (!mapped_grouping_plan(a.R, a.N, &G, &nb)) return hipErrorInvalidValue;
+  char* ws = static_cast<char*>(a.workspace);
+  int32_t* grp_off = reinterpret_cast<int32_t*>(ws);
+  int32_t* order = reinterpret_cast<int32_t*>(ws + align_up256((size_t)(a.R + 1) * 4));
+  int32_t* hist = reinterpret_cast<int32_t*>(ws + align_up256((size_t)(a.R + 1) * 4) +
+                                             align_up256((size_t)a.N * 4));
+  hipError_t e = launch_kernel(group_count, dim3((uint32_t)nb), dim3(256), s, a.ids, a.N,
+                               (int)a.R, G, nb, hist);
+  if (e == hipSuccess)
+    e = launch_kernel(group_scan, dim3(1), dim3(1024), s, hist, a.R * (int64_t)nb, (int)a.R, nb,
+                      a.N, grp_off);
+  if (e == hipSuccess)
+    e = launch_kernel(group_scatter, dim3((uint32_t)nb), dim3(64), s, a.ids, a.N, (int)a.R, G,
+                      nb, static_cast<const int32_t*>(hist), order);
+  if (e != hipSuccess) return e;
+  return launch_fast<D, true>(a, grp_off, order, s);
 }
 
 template <typename T>
@@ -524,11 +660,34 @@ hipError_t launch_generic(const AttentionArgs& a, hipStream_t s) {
 
 }  // namespace
 
+bool mapped_grouping_plan(int64_t R, int64_t N, int64_t* G, int* nb) {
+  if (R < 1 || R > kGroupMaxRequests || N < 1) return false;
+  int64_t g = 4096;
+  while (R * ((N + g - 1) / g) > kGroupMaxHist && g < (int64_t(1) << 24)) g *= 2;
+  const int64_t blocks = (N + g - 1) / g;
+  if (R * blocks > kGroupMaxHist || blocks >= (int64_t(1) << 31)) return false;
+  *G = g;
+  *nb = (int)blocks;
+  return true;
+}
+
+size_t mapped_grouping_bytes(int64_t R, int64_t N) {
+  int64_t G = 0;
+  int nb = 0;
+  if (!mapped_grouping_plan(R, N, &G, &nb)) return 0;
+  return align_up256((size_t)(R + 1) * 4) + align_up256((size_t)N * 4) +
+         align_up256((size_t)R * (size_t)nb * 4);
+}
+
 hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s) {
-  // The tiled kernel needs the candidates of a request contiguous (CSR); a
-  // caller's per-candidate map runs the general kernel.
+  // The tiled kernel runs on request-contiguous candidates: the CSR offsets,
+  // or a caller's per-candidate map grouped by request first (that needs the
+  // grouping workspace); otherwise the general kernel runs.
   if (fast && a.ids == nullptr)
-    return a.head_dim == 128 ? launch_fast<128>(a, s) : launch_fast<64>(a, s);
+    return a.head_dim == 128 ? launch_fast<128, false>(a, a.cand_offsets, nullptr, s)
+                             : launch_fast<64, false>(a, a.cand_offsets, nullptr, s);
+  if (fast && a.workspace != nullptr)
+    return a.head_dim == 128 ? launch_fast_mapped<128>(a, s) : launch_fast_mapped<64>(a, s);
   return a.bf16 ? launch_generic<bf16_t>(a, s) : launch_generic<float>(a, s);
 }
 

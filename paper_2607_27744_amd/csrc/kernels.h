@@ -41,6 +41,7 @@ struct AttentionArgs {
   bool bf16;
   void* out;
   const int32_t* ids;  // caller's per-candidate request map, or NULL (CSR offsets)
+  void* workspace;     // grouping workspace of the mapped form (mapped_grouping_bytes), or NULL
 };
 
 struct InteractionArgs {
@@ -111,6 +112,11 @@ hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t*
                               hipStream_t s);
 hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s);
 hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s);
+// Grouping of a per-candidate map by request for the tiled attention kernel:
+// false when R or the per-block count table is too large for it (then the
+// general kernel runs); the workspace it needs, 0 in that case.
+bool mapped_grouping_plan(int64_t R, int64_t N, int64_t* G, int* nb);
+size_t mapped_grouping_bytes(int64_t R, int64_t N);
 hipError_t launch_interaction(const InteractionArgs& a, bool fast, hipStream_t s);
 hipError_t launch_lcb(const LcbArgs& a, bool fast, hipStream_t s);
 bool lcb_fast_shape(int f_cand, int o_cand, int emb);

@@ -16,7 +16,8 @@ from . import _lib
 __all__ = [
     "load_library", "ikbo_linear", "ikbo_linear_mapped", "glm_linear", "ikbo_linear_combined",
     "linear_workspace_size", "pad_dims",
-    "dca_attention", "dca_attention_mapped", "dca_request_attention", "glm_interaction",
+    "dca_attention", "dca_attention_mapped", "dca_attention_mapped_workspace_size",
+    "dca_request_attention", "glm_interaction",
     "ikbo_lcb", "ikbo_lcb_mapped", "ikbo_mlp2", "mlp2_workspace_size", "glm_fm_linear",
     "fm_linear_workspace_size", "request_ids",
     "validate_offsets", "RocsError",
@@ -351,11 +352,19 @@ def dca_attention(q, k, v, cand_offsets, kv_offsets, *, scale=None, out=None, st
     return _attention(q, k, v, cand_offsets, None, kv_offsets, scale, out, stream)
 
 
+def dca_attention_mapped_workspace_size(num_requests, num_cand):
+    return int(_lib.load().rocs_dca_attention_mapped_workspace_size(num_requests, num_cand))
+
+
 def dca_attention_mapped(q, k, v, cand_request_ids, kv_offsets, *, scale=None, out=None,
-                         stream=None):
+                         workspace=None, stream=None):
     """rocs_dca_attention_mapped: as dca_attention, with m given per candidate
-    (cand_request_ids int32 [N], each in [0, R) with R = kv_offsets.numel() - 1)."""
-    return _attention(q, k, v, None, cand_request_ids, kv_offsets, scale, out, stream)
+    (cand_request_ids int32 [N], each in [0, R) with R = kv_offsets.numel() - 1).
+    The workspace (allocated here when not given) receives the grouping of the
+    candidates by request: grp_off [R + 1] int32 at offset 0, then order [N]
+    int32 at the next 256-byte boundary."""
+    return _attention(q, k, v, None, cand_request_ids, kv_offsets, scale, out, stream,
+                      workspace=workspace)
 
 
 def dca_request_attention(q_req, k, v, kv_offsets, *, scale=None, out=None, stream=None):
@@ -380,7 +389,7 @@ def _identity_offsets(n_req, device):
     return _IDENTITY[key]
 
 
-def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream):
+def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream, workspace=None):
     lib = _lib.load()
     mapped = cand_ids is not None
     _need(q.dim() == 4 and q.is_contiguous(), "q must be a contiguous [N, T, H, d] tensor")
@@ -404,12 +413,21 @@ def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream):
           "out must match q")
     _on_gpu(q, k, v, cand_offsets, cand_ids, kv_offsets, out)
     stride = k.stride(0) if k.shape[0] > 1 else heads * dim
-    fn, name = ((lib.rocs_dca_attention_mapped, "rocs_dca_attention_mapped") if mapped
-                else (lib.rocs_dca_attention, "rocs_dca_attention"))
-    _lib.check(fn(
-        _ptr(q), _ptr(k), _ptr(v), _ptr(cand_ids if mapped else cand_offsets), _ptr(kv_offsets),
-        n_req, n_cand, q_len, heads, dim, stride, float(scale or 0.0), _dtype_code(q),
-        _ptr(out), _stream(stream)), name)
+    if mapped:
+        need = int(lib.rocs_dca_attention_mapped_workspace_size(n_req, n_cand))
+        if workspace is None and need > 0:
+            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        _on_gpu(workspace)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        _lib.check(lib.rocs_dca_attention_mapped(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(cand_ids), _ptr(kv_offsets), n_req, n_cand, q_len,
+            heads, dim, stride, float(scale or 0.0), _dtype_code(q), _ptr(out), _ptr(workspace),
+            ws_bytes, _stream(stream)), "rocs_dca_attention_mapped")
+        return out
+    _lib.check(lib.rocs_dca_attention(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(cand_offsets), _ptr(kv_offsets), n_req, n_cand, q_len,
+        heads, dim, stride, float(scale or 0.0), _dtype_code(q), _ptr(out), _stream(stream)),
+        "rocs_dca_attention")
     return out
 
 

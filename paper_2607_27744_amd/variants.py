@@ -13,6 +13,9 @@ line with the call's algorithmic FLOPs and bytes against the MI355X peaks.
   dca_tq32          DCA with 32-token candidate queries (Section 4.3.2):
                     16 requests x 512 candidates, history 2048, 8 heads x 128
   dca_tq64          the same with 64-token queries, 256 candidates per request
+  dca_mapped        the dca_tq32 shape with the candidates shuffled and m given
+                    per candidate (grouped by request on the device, then the
+                    tiled kernel), timed beside the CSR call on the same rows
   dca_request       request-side cross attention (identity map): 16 requests,
                     32 query tokens each, history 2048, 8 heads x 128
   linear_mapped     the retrieval-MLP first layer (64 requests, ~65k
@@ -45,7 +48,8 @@ from . import workloads as wl
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 
-NAMES = ("lcb", "dca_tq32", "dca_tq64", "dca_request", "linear_mapped", "linear_combined",
+NAMES = ("lcb", "dca_tq32", "dca_tq64", "dca_mapped", "dca_request", "linear_mapped",
+         "linear_combined",
          "glm_linear", "dca_layer", "mlp2", "fm_linear")
 
 
@@ -130,6 +134,29 @@ def _dca(name, r, n_r, q_len, steps, warmup, request_side=False):
     return _line(name, {"requests": r, "candidates_per_request": n_r, "q_len": q_len,
                         "history": length, "heads": h, "head_dim": d},
                  ms, flops, byts, "mfma", n, "candidates")
+
+
+def _dca_mapped(steps, warmup):
+    r, n_r, q_len, h, d, length = 16, 512, 32, 8, 128, 2048
+    c = wl.attention_case([n_r] * r, [length] * r, h, d, q_len=q_len, seed=2)
+    perm = np.random.default_rng(7).permutation(r * n_r)
+    m = _request_map(c.cand_offsets)[perm]
+    q, k, v = _bf16(c.q[perm]), _bf16(c.k), _bf16(c.v)
+    kv_off, ids, co = _i32(c.kv_offsets), _i32(m), _i32(c.cand_offsets)
+    out = torch.empty_like(q)
+    ws = torch.empty(max(ops.dca_attention_mapped_workspace_size(r, r * n_r), 1),
+                     dtype=torch.uint8, device="cuda")
+    ms = _time(lambda: ops.dca_attention_mapped(q, k, v, ids, kv_off, out=out, workspace=ws),
+               steps, warmup)
+    qc = _bf16(c.q)
+    ms_csr = _time(lambda: ops.dca_attention(qc, k, v, co, kv_off, out=out), steps, warmup)
+    n = r * n_r
+    flops = 4.0 * n * q_len * length * h * d
+    byts = 2.0 * (2 * n * q_len * h * d + 2 * r * length * h * d) + 4.0 * n
+    return _line("dca_mapped", {"requests": r, "candidates_per_request": n_r, "q_len": q_len,
+                                "history": length, "heads": h, "head_dim": d,
+                                "order": "shuffled"},
+                 ms, flops, byts, "mfma", n, "candidates", {"csr_ms": round(ms_csr, 4)})
 
 
 def _linear_l1_case():
@@ -290,6 +317,8 @@ def run(name, steps=20, warmup=3):
         return _dca(name, 16, 512, 32, steps, warmup)
     if name == "dca_tq64":
         return _dca(name, 16, 256, 64, steps, warmup)
+    if name == "dca_mapped":
+        return _dca_mapped(steps, warmup)
     if name == "dca_request":
         return _dca(name, 16, 1, 32, steps, warmup, request_side=True)
     if name == "linear_mapped":

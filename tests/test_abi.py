@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 21
+    assert len(names) == 22
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -121,13 +121,31 @@ def test_mapped_entry_points_argument_errors(lib):
 
     def att(**kw):
         a = dict(q=FAKE[0], k=FAKE[1], v=FAKE[2], ids=FAKE[3], ko=FAKE[4], R=2, N=4, T=1, H=2,
-                 d=64, stride=0, scale=0.0, dtype=1, out=FAKE[5], stream=None)
+                 d=64, stride=0, scale=0.0, dtype=1, out=FAKE[5], ws=FAKE[6], ws_bytes=1 << 20,
+                 stream=None)
         a.update(kw)
         return lib.rocs_dca_attention_mapped(*a.values())
     assert att(ids=None) == _lib.INVALID_ARGUMENT
     assert att(ko=None) == _lib.INVALID_ARGUMENT
     assert att(T=0) == _lib.INVALID_ARGUMENT
     assert att(N=0) == _lib.OK
+    # The tiled path (bf16, head_dim 64) groups in the workspace: it is required.
+    assert att(ws=None) == _lib.WORKSPACE_TOO_SMALL
+    assert att(ws_bytes=8) == _lib.WORKSPACE_TOO_SMALL
+    assert att(ws=P(0x70010)) == _lib.INVALID_ARGUMENT          # not 256-aligned
+    # fp32 runs the general kernel, which needs none.
+    assert att(dtype=0, ws=None, N=0) == _lib.OK
+
+
+def test_mapped_attention_workspace_size(lib):
+    # grp_off [R + 1] and order [N] int32, then the per-block counts [R x
+    # ceil(N / 4096)], each 256-byte aligned; zero where the grouping does
+    # not apply (more than 16384 requests).
+    f = lib.rocs_dca_attention_mapped_workspace_size
+    assert f(4, 1000) == 256 + 4096 + 256
+    assert f(16, 1 << 20) == 256 + (1 << 22) + 16 * 256 * 4
+    assert f(0, 10) == 0 and f(3, 0) == 0
+    assert f(20000, 100) == 0
 
 
 @no_gpu

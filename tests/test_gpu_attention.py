@@ -158,6 +158,43 @@ def test_mapped_attention_index_probe_bit_exact(gpu_lib, head_dim, bf16):
 
 
 @pytest.mark.parametrize("head_dim", [64, 128])
+def test_mapped_grouping_and_tiled_parity(gpu_lib, head_dim):
+    # The mapped form groups the candidates by request on the device (a
+    # stable counting sort over blocks of 4096 candidates) and runs the tiled
+    # kernel in grouped order. The grouping left in the workspace must be
+    # NumPy's stable argsort of the map and the offsets of its counts, bit
+    # for bit; the outputs match the oracle. About 14k candidates (four
+    # grouping blocks), 41 requests of which three are empty, one with a
+    # single candidate, histories of 1 .. 300 rows, two query tokens.
+    rng = np.random.default_rng(head_dim)
+    counts = rng.integers(150, 600, size=41)
+    counts[[4, 17, 30]] = 0
+    counts[9] = 1
+    lens = rng.integers(1, 300, size=41)
+    case = wl.attention_case(counts, lens, 2, head_dim, q_len=2, seed=80 + head_dim)
+    n = case.q.shape[0]
+    perm = rng.permutation(n)
+    m = ikbo.request_ids(case.cand_offsets)[perm].astype(np.int32)
+    q = np.ascontiguousarray(case.q[perm])
+    ws = torch.zeros(ops.dca_attention_mapped_workspace_size(41, n), dtype=torch.uint8,
+                     device="cuda")
+    got = host(ops.dca_attention_mapped(dev_bf16(q), dev_bf16(case.k), dev_bf16(case.v),
+                                        dev_i32(m), dev_i32(case.kv_offsets), workspace=ws))
+    want = ikbo.dca_attention(q, case.k, case.v, None, case.kv_offsets, request_map=m)
+    assert_close(got, round_bf16(want), f"mapped tiled d{head_dim}")
+    raw = ws.cpu().numpy().view(np.int32)
+    grp_off = raw[:42]
+    order = raw[256 // 4 * ((42 * 4 + 255) // 256):][:n]
+    np.testing.assert_array_equal(order, np.argsort(m, kind="stable"))
+    np.testing.assert_array_equal(grp_off, np.concatenate([[0], np.cumsum(np.bincount(m, minlength=41))]))
+    # Every row equals the CSR kernel's row for the same candidate: grouping
+    # only reorders which rows share a tile.
+    csr = host(ops.dca_attention(dev_bf16(case.q), dev_bf16(case.k), dev_bf16(case.v),
+                                 dev_i32(case.cand_offsets), dev_i32(case.kv_offsets)))
+    np.testing.assert_array_equal(got, csr[perm])
+
+
+@pytest.mark.parametrize("head_dim", [64, 128])
 @pytest.mark.parametrize("q_len", [1, 32])
 def test_request_side_attention(gpu_lib, head_dim, q_len):
     # A^R = Attn(Q^R, K, V): each request's own queries over its history
