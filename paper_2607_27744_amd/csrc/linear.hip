@@ -279,17 +279,24 @@ void ikbo_gemm_bf16(
 // Persistent workgroups, one per CU, walk the 256 (features) x 256
 // (candidates) output tiles with a stride of the grid; eight waves, two per
 // SIMD, each own a 64 x 128 block (8 MFMA 32x32 accumulators, 128 of the
-// wave's 256 registers), so one wave's stalls (slab waits, fragment reads,
-// the epilogue's stores) leave the SIMD to the other. K arrives in 64-wide slabs (128-byte row segments:
-// whole cache lines, which the L2 serves at twice the rate of half lines)
-// through LDS rings filled by LDS DMA loads, as one stream across tile
-// boundaries: the weight slab (L2-resident) one slab ahead of use in a
-// 2-deep ring, the candidate slab (from HBM, longer latency) two slabs ahead
-// in a 3-deep ring; together exactly the 160 KiB of LDS. The loads are
-// issued one at a time between the MFMAs. The 16-byte chunks of each slab
-// row are XOR-swizzled by (row / 2) % 8, which puts the 16 rows read by each
-// quarter-wave on distinct banks; fragments are read one k-step ahead.
+// wave's 256 registers), so one wave's stalls (fragment reads, the
+// epilogue's stores) leave the SIMD to the other. K arrives in 64-wide slabs
+// (128-byte row segments: whole cache lines, which the L2 serves at twice the
+// rate of half lines) through LDS rings filled by LDS DMA loads, as one
+// stream across tile boundaries: the weight slab (L2-resident) one slab ahead
+// of use in a 2-deep ring, the candidate slab (from HBM, longer latency) two
+// slabs ahead in a 3-deep ring; together exactly the 160 KiB of LDS. The
+// 16-byte chunks of each slab row are XOR-swizzled by (row / 2) % 8, which
+// puts the 16 rows read by each quarter-wave on distinct banks; fragments
+// are read one k-step ahead.
 //
+// Producer waves: waves 0-3 issue every DMA load (two pieces between
+// consecutive MFMA groups), waves 4-7 none. The two waves of a SIMD do not
+// progress alike (the arbiter favours the older one, waves 0-3), so loads
+// issued by the slower waves arrived late and the whole workgroup waited at
+// the slab barrier for them; the faster waves have that time to spare. Each
+// wave waits only for its own loads (the vector-memory counter is per wave),
+// so waves 4-7 never wait on a load of the ring.
 // IKBO tiling (Section 4.2.1): with a request term, tiles never straddle two
 // requests: request r owns tile slots r + floor(off[r] / 256) ... (the last
 // one partial), so the whole tile shares one row of the request table
@@ -298,8 +305,14 @@ void ikbo_gemm_bf16(
 // contiguously and Zb is the bias (or absent).
 //
 // Epilogue: Zb, activation on packed bf16, then the two wave halves swap
-// 8-byte pieces so every lane holds 8 consecutive features: 16-byte stores,
-// which drain while the next tile computes.
+// 8-byte pieces so every lane holds 8 consecutive features of one row. Stored
+// from that layout, each instruction would write 32 bytes into each of 32
+// rows, and a CU then stores at about a quarter of the rate it reaches with
+// whole 128-byte lines (measured on this part: ~38 GB/s against ~150 GB/s
+// per CU). So each wave passes its block through 4 KiB of the candidate slot
+// the last slab has just released (after a barrier): 32 rows at a time
+// written in that layout, read back row-contiguous, and stored as 8 rows x
+// 128 bytes per instruction.
 //
 // Rows past the tile's end are clamped loads whose results are not stored.
 // ---------------------------------------------------------------------------
@@ -451,15 +464,24 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   const int first = FUSED ? (int)gridDim.x - 1 - logical : logical;
   const uint32_t lbase = lds_addr(lds);
 
-  // DMA lane map: load i of this wave fills slab rows RPI (NI wave + i) +
-  // lane / 8, chunk position lane % 8, with chunk (lane % 8) ^ ((row / 2) % 8).
-  // Rows past the operand's valid rows are clamped to the last valid one.
-  const int drow0 = RPI * NI * wave + (lane >> 3);
+  // DMA lane map (producer waves 0-3): load i of this wave fills slab rows
+  // RPI (PI wave + i) + lane / 8, chunk position lane % 8, with chunk
+  // (lane % 8) ^ ((row / 2) % 8). Rows past the operand's valid rows are
+  // clamped to the last valid one.
+  constexpr int PI = 2 * NI;                     // DMA loads per producer wave and operand (8)
+  const bool producer = wave < 4;
+  const int drow0 = RPI * PI * (wave & 3) + (lane >> 3);
   auto dma_piece = [&](const char* src, int rowlim, uint32_t dst, int i) __attribute__((always_inline)) {
     const int row = drow0 + RPI * i;
     const uint32_t chunk = 16u * (uint32_t)((lane & 7) ^ ((row >> 1) & 7));
     lds_dma16_sv(src, (uint32_t)(min(row, rowlim) * rowb) + chunk,
-                 dst + (uint32_t)(RPI * (NI * wave + i) * ROWB));
+                 dst + (uint32_t)(RPI * (PI * (wave & 3) + i) * ROWB));
+  };
+  auto dma_all = [&](const char* src, int rowlim, uint32_t dst) __attribute__((always_inline)) {
+    if (producer) {
+#pragma unroll
+      for (int i = 0; i < PI; ++i) dma_piece(src, rowlim, dst, i);
+    }
   };
 
   // The issue cursor walks the slab sequence two slabs ahead of compute and
@@ -506,12 +528,20 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     buf_a ^= 1;
     a_queued = false;
   };
-  // Piece p of the planned loads: weights 0..NI-1, candidates NI..2NI-1.
+  // Group p (0..7) of the planned loads, two pieces each: weights for
+  // p < 4, candidates after.
   auto dma_plan_piece = [&](int p) __attribute__((always_inline)) {
+    if (!producer) return;
     if (p < NI) {
-      if (pa_on) dma_piece(pa_src, pa_lim, pa_dst, p);
+      if (pa_on) {
+        dma_piece(pa_src, pa_lim, pa_dst, 2 * p);
+        dma_piece(pa_src, pa_lim, pa_dst, 2 * p + 1);
+      }
     } else {
-      if (pb_on) dma_piece(pb_src, pb_lim, pb_dst, p - NI);
+      if (pb_on) {
+        dma_piece(pb_src, pb_lim, pb_dst, 2 * (p - NI));
+        dma_piece(pb_src, pb_lim, pb_dst, 2 * (p - NI) + 1);
+      }
     }
   };
 
@@ -647,18 +677,34 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   // whose extent ends after the tile's last candidate row, so stores of rows
   // past it are dropped. A tile that reaches past feature D (D not a
   // multiple of the tile) tests each store.
-  auto store_tile = [&](const StreamTile& c) __attribute__((always_inline)) {
+  // `stage` is this wave's 4 KiB of free LDS. Staging layout: row r (of the
+  // 32 candidates of one fn block) at r * 128 bytes, its 16-byte chunk c
+  // (features 8 c .. 8 c + 7 of the wave's 64) at position c ^ (r % 8), so
+  // both the writes (32 rows at one chunk) and the row-contiguous reads
+  // (8 rows x 8 chunks) spread over all banks.
+  auto store_tile = [&](const StreamTile& c, uint32_t stage) __attribute__((always_inline)) {
     if (c.m0 + BM <= D) {
       const auto ro = buffer_rsrc(out + c.n0 * D, (uint32_t)c.rows * (uint32_t)D * 2u);
-      const uint32_t vo = 2u * ((uint32_t)(wn0 + l32) * (uint32_t)D + (uint32_t)(c.m0 + wm0 + 8 * hh));
+      ROCS_LDS char* const st = lds3 + stage;
+      const int rr = lane >> 3, cr = lane & 7;  // read-back: row 8 i + rr, chunk cr
+      const uint32_t vo = 2u * ((uint32_t)(wn0 + rr) * (uint32_t)D + (uint32_t)(c.m0 + wm0 + 8 * cr));
 #pragma unroll
       for (int fn = 0; fn < 4; ++fn) {
-        const uint32_t vr = vo + 64u * (uint32_t)fn * (uint32_t)D;
 #pragma unroll
         for (int fm = 0; fm < 2; ++fm)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            __builtin_amdgcn_raw_buffer_store_b128(swapped(fm, fn, j), ro, vr + 2u * (32 * fm + 16 * j), 0, 0);
+          for (int j = 0; j < 2; ++j) {
+            const int ch = 4 * fm + 2 * j + hh;
+            *reinterpret_cast<ROCS_LDS u32x4*>(st + l32 * 128 + 16 * (ch ^ (l32 & 7))) =
+                swapped(fm, fn, j);
+          }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = 8 * i + rr;
+          const u32x4 v = *reinterpret_cast<const ROCS_LDS u32x4*>(st + r * 128 + 16 * (cr ^ (r & 7)));
+          __builtin_amdgcn_raw_buffer_store_b128(
+              v, ro, vo + 2u * (uint32_t)(32 * fn + 8 * i) * (uint32_t)D, 0, 0);
+        }
       }
       return;
     }
@@ -688,26 +734,26 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   StreamTile cc = ic;
   plan_b();
   plan_a();
-#pragma unroll
-  for (int i = 0; i < NI; ++i) {
-    dma_piece(pb_src, pb_lim, pb_dst, i);
-    dma_piece(pa_src, pa_lim, pa_dst, i);
-  }
+  dma_all(pb_src, pb_lim, pb_dst);
+  dma_all(pa_src, pa_lim, pa_dst);
   if (ic_live) {
     plan_b();
-#pragma unroll
-    for (int i = 0; i < NI; ++i) dma_piece(pb_src, pb_lim, pb_dst, i);
+    dma_all(pb_src, pb_lim, pb_dst);
   }
   pa_on = pb_on = false;
   if constexpr (FUSED) wait_request_side();   // while the first slabs load
   wait_vmcnt<0>();
   ring_barrier();
 
-  // One slab. Vector-memory operations retire in issue order. In an inner
-  // slab the candidate loads (slab g + 2) follow the weight loads (g + 1),
-  // so waiting until only those are in flight makes slab g + 1 resident. In
-  // the last slab of a tile the candidates of slab g + 2 wait until after
-  // the epilogue, and the Zb loads are issued and drained with the slab.
+  // One slab. Vector-memory operations retire in issue order (the
+  // counter of outstanding ones is decremented in order), and only the
+  // producer waves have ring loads in flight. In an inner slab the candidate
+  // loads (slab g + 2) follow the weight loads (g + 1), so waiting until only
+  // those are in flight makes slab g + 1 resident. In the last slab of a
+  // tile the candidates of slab g + 2 wait until after the epilogue, and the
+  // Zb loads are issued and drained with the slab; the epilogue stages
+  // through the candidate slot the slab has just released, once every wave
+  // is done with it.
   auto step = [&](auto first_slab, auto last_slab) __attribute__((always_inline)) {
     constexpr bool kLast = decltype(last_slab)::value;
     const bool a_next = a_queued;
@@ -716,20 +762,23 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     if (!kLast && b_next) plan_b();
     compute(first_slab);
     pa_on = pb_on = false;
+    const uint32_t released = (uint32_t)(BBASE + cbuf_b * SLAB);
     cbuf_a ^= 1;
     cbuf_b = cbuf_b == NSB - 1 ? 0 : cbuf_b + 1;
     if constexpr (kLast) {
+      ring_barrier();                            // every wave is past the slab's fragments
       load_zb(cc);
       wait_vmcnt<0>();
-      store_tile(cc);
+      store_tile(cc, released + (uint32_t)wave * 4096u);
       if (b_next) {
         plan_b();
-#pragma unroll
-        for (int i = 0; i < NI; ++i) dma_piece(pb_src, pb_lim, pb_dst, i);
+        dma_all(pb_src, pb_lim, pb_dst);
         pb_on = false;
       }
     } else {
-      if (b_next) wait_vmcnt<NI>(); else wait_vmcnt<0>();
+      if (producer) {
+        if (b_next) wait_vmcnt<PI>(); else wait_vmcnt<0>();
+      }
     }
     if (a_next) ring_barrier();                  // a next slab exists
   };
