@@ -474,7 +474,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   auto dma_piece = [&](const char* src, int rowlim, uint32_t dst, int i) __attribute__((always_inline)) {
     const int row = drow0 + RPI * i;
     const uint32_t chunk = 16u * (uint32_t)((lane & 7) ^ ((row >> 1) & 7));
-    lds_dma16_sv(src, (uint32_t)(min(row, rowlim) * rowb) + chunk,
+    lds_dma16_sv(src, __umul24((uint32_t)min(row, rowlim), (uint32_t)rowb) + chunk,
                  dst + (uint32_t)(RPI * (PI * (wave & 3) + i) * ROWB));
   };
   auto dma_all = [&](const char* src, int rowlim, uint32_t dst) __attribute__((always_inline)) {
@@ -550,12 +550,20 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
   const uint32_t fa0 = (uint32_t)(l32 * ROWB + 16 * (hh ^ ((l32 >> 1) & 7)));
   f32x16 acc[2][4];
   int cbuf_a = 0, cbuf_b = 0;            // ring slots of the slab being computed
-  auto compute = [&](auto first_slab) __attribute__((always_inline)) {
+  // Fragments, double-buffered across k-steps (slot ks % 2): the reads of
+  // step ks + 1 are in flight while the MFMAs of step ks run. The last
+  // k-step of a slab that is not a tile's last is deferred: its fragments
+  // are read (and waited for) before the slab barrier, and its MFMAs run
+  // after the barrier, while the next slab's first fragment reads are in
+  // flight; every wave would otherwise start each slab waiting for LDS. The
+  // accumulation order is unchanged.
+  bf16x8 af[2][2], bfr[2][4];
+  auto compute = [&](auto first_slab, auto last_slab) __attribute__((always_inline)) {
+    constexpr bool kFirst = decltype(first_slab)::value;
+    constexpr bool kLastS = decltype(last_slab)::value;
+    constexpr int KSTEPS = BK / 16;
     const uint32_t sa = (uint32_t)(cbuf_a * SLAB) + wm0 * ROWB;
     const uint32_t sb = (uint32_t)(BBASE + cbuf_b * SLAB) + wn0 * ROWB;
-    // Fragments double-buffered across k-steps: the reads of step ks + 1 are
-    // in flight while the MFMAs of step ks run.
-    bf16x8 af[2][2], bfr[2][4];
     auto load_frags = [&](int ks, int slot) __attribute__((always_inline)) {
 #pragma unroll
       for (int f = 0; f < 4; ++f) {
@@ -563,17 +571,30 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
         bfr[slot][f] = *reinterpret_cast<const ROCS_LDS bf16x8*>(lds3 + sb + 32 * f * ROWB + (fa0 ^ (32u * ks)));
       }
     };
+    // DMA group g (0..7) goes with the g-th MFMA group of the slab.
+    constexpr int kDeferred = kFirst ? 0 : 2;          // MFMA groups of the previous slab
     load_frags(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (!kFirst) {
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
+      for (int fm = 0; fm < 2; ++fm) {
+#pragma unroll
+        for (int fn = 0; fn < 4; ++fn) acc[fm][fn] = mfma32(af[1][fm], bfr[1][fn], acc[fm][fn]);
+        dma_plan_piece(fm);
+        __builtin_amdgcn_sched_barrier(0x0002 | 0x0004);
+      }
+    }
+    constexpr int KRUN = kLastS ? KSTEPS : KSTEPS - 1;
+#pragma unroll
+    for (int ks = 0; ks < KRUN; ++ks) {
       const int cur = ks & 1;
-      if (ks + 1 < BK / 16) load_frags(ks + 1, cur ^ 1);
+      if (ks + 1 < KSTEPS) load_frags(ks + 1, cur ^ 1);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int fm = 0; fm < 2; ++fm) {
 #pragma unroll
         for (int fn = 0; fn < 4; ++fn) {
-          if constexpr (decltype(first_slab)::value) {
+          if constexpr (kFirst) {
             if (ks == 0) {
               const f32x16 zero = {};
               acc[fm][fn] = mfma32(af[cur][fm], bfr[cur][fn], zero);
@@ -582,11 +603,16 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
           }
           acc[fm][fn] = mfma32(af[cur][fm], bfr[cur][fn], acc[fm][fn]);
         }
-        dma_plan_piece(2 * ks + fm);
+        if (kDeferred + 2 * ks + fm < 8) dma_plan_piece(kDeferred + 2 * ks + fm);
         // Keep MFMAs and loads in this order; ALU work may move.
         __builtin_amdgcn_sched_barrier(0x0002 | 0x0004);
       }
     }
+#pragma unroll
+    for (int g = kDeferred + 2 * KRUN; g < 8; ++g) dma_plan_piece(g);
+    // The deferred step's fragments are in registers before the barrier
+    // hands this slab's ring slots to the next loads.
+    if constexpr (!kLastS) wait_lgkmcnt0();
   };
 
   // Request row Zb[m0 + wm0 + 32 fm + 8 q + h4 .. +3] of the tile, loaded
@@ -760,7 +786,7 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
     if (a_next) plan_a();
     const bool b_next = ic_live;
     if (!kLast && b_next) plan_b();
-    compute(first_slab);
+    compute(first_slab, last_slab);
     pa_on = pb_on = false;
     const uint32_t released = (uint32_t)(BBASE + cbuf_b * SLAB);
     cbuf_a ^= 1;
