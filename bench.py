@@ -93,10 +93,11 @@ def op_plan(w):
         att = _attention_work(w.n_cand, 1, 4, 64, list(zip(counts, lens)))
         kv = _linear_work(0, l_tot, 0, 256, 512)
         q = _linear_work(0, w.n_cand, 0, 256, 256)
-        q2 = _linear_work(0, w.n_cand, 0, 256, 256, add=True)
+        # Layer 1's attention also reads e_c and writes u = round(A1 + e_c).
+        att_res = (att[0], att[1] + 2 * 2 * w.n_cand * 256)
         return [("kv_projection_l1", *kv, "hbm"), ("q_projection_l1", *q, "hbm"),
-                ("dca_attention_l1", *att, "hbm"), ("kv_projection_l2", *kv, "hbm"),
-                ("q_projection_l2", *q2, "hbm"), ("dca_attention_l2", *att, "hbm")]
+                ("dca_attention_l1", *att_res, "hbm"), ("kv_projection_l2", *kv, "hbm"),
+                ("q_projection_l2", *q, "hbm"), ("dca_attention_l2", *att, "hbm")]
     if cid == 4:
         # The interaction feeds the linear's operand on chip: Y^C never reaches HBM.
         ff, _ = _fm_work(w.n_req, w.n_cand, 32, 8, 128)
@@ -115,45 +116,9 @@ def op_plan(w):
 
 
 def timed_step_fns(p):
-    """The step split into its operator calls (same calls as pipelines.step)."""
-    from paper_2607_27744_amd import ops, pipelines
-    cid = p.config_id
-    n = p.n_cand
-    kvv = pipelines._kv_views
-    if cid == 1:
-        return [lambda: ops.ikbo_linear(p.x_cand, p.w_cand, x_req=p.x_req, w_req=p.w_req,
-                                        cand_offsets=p.cand_offsets, activation="relu",
-                                        out=p.linear, workspace=p.ws),
-                lambda: ops.dca_attention(p.q, p.k, p.v, p.cand_offsets, p.kv_offsets,
-                                          out=p.attention)]
-    if cid == 2:
-        return [lambda: pipelines.step(p)]
-    if cid == 3:
-        def att(q, kv, o):
-            k, v = kvv(kv, p.h, p.d)
-            return ops.dca_attention(q.view(n, 1, p.h, p.d), k, v, p.cand_offsets,
-                                     p.kv_offsets, out=o)
-        return [lambda: ops.ikbo_linear(p.s, p.wkv1, out=p.kv1),
-                lambda: ops.ikbo_linear(p.e_c, p.wq1, out=p.q1),
-                lambda: att(p.q1, p.kv1, p.a1),
-                lambda: ops.ikbo_linear(p.s, p.wkv2, out=p.kv2),
-                lambda: ops.ikbo_linear(p.a1.view(n, p.h * p.d), p.wq2, x_cand_add=p.e_c,
-                                        out=p.q2),
-                lambda: att(p.q2, p.kv2, p.a2)]
-    if cid == 4:
-        return [lambda: pipelines.step(p)]
-    if cid == 5:
-        def att():
-            k, v = kvv(p.kv, p.h, p.d)
-            return ops.dca_attention(p.h1.view(n, 1, p.h, p.d), k, v, p.cand_offsets,
-                                     p.kv_offsets, out=p.attention)
-        return [lambda: ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
-                                        cand_offsets=p.cand_offsets, activation="relu",
-                                        out=p.h1, workspace=p.ws),
-                lambda: ops.ikbo_linear(p.h1, p.w2, out=p.out2),
-                lambda: ops.ikbo_linear(p.s, p.wkv, out=p.kv),
-                att]
-    raise ValueError(cid)
+    """The step split into its operator calls (the calls pipelines.step makes)."""
+    from paper_2607_27744_amd import pipelines
+    return pipelines.step_calls(p)
 
 
 _OP_KERNEL = (("dca_attention", "dca_attn_bf16"), ("glm_interaction", "glm_fm_bf16"),

@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define ROCS_ABI_VERSION 2
+#define ROCS_ABI_VERSION 3
 
 typedef enum rocs_status {
   ROCS_OK = 0,
@@ -290,6 +290,35 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
                            int32_t q_len, int32_t num_heads, int32_t head_dim,
                            int64_t kv_row_stride, float softmax_scale, int32_t dtype,
                            void* out, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_dca_attention_residual: rocs_dca_attention that also emits the
+ * pointwise residual that feeds the next layer of stacked DCA (Section 3.2:
+ * the next layer's query input is this layer's output plus the candidate
+ * embedding; a pointwise operation, so GLM-compliant, Eq. glm-elementwise):
+ *
+ *   out_sum[n][t][h][e] = round(out[n][t][h][e] + residual[n][t][h][e])
+ *
+ * where out is first rounded to dtype (exactly the values written to out),
+ * the sum is taken in fp32 and rounded to dtype (round to nearest even;
+ * no rounding for fp32). The sum is formed in the attention's epilogue, so
+ * the next projection reads one tensor instead of two.
+ *
+ *   residual  [N, q_len, H, head_dim], the layout of q (device memory)
+ *   out_sum   [N, q_len, H, head_dim], must not overlap any input or out
+ * Every other argument, the result and the errors are those of
+ * rocs_dca_attention (the fast path also needs residual and out_sum 16-byte
+ * aligned). An empty history gives out = 0 and out_sum = residual.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_dca_attention_residual(const void* q, const void* k, const void* v,
+                                    const int32_t* cand_offsets, const int32_t* kv_offsets,
+                                    int64_t num_requests, int64_t num_cand,
+                                    int32_t q_len, int32_t num_heads, int32_t head_dim,
+                                    int64_t kv_row_stride, float softmax_scale, int32_t dtype,
+                                    const void* residual, void* out, void* out_sum,
+                                    void* stream);
 
 /*
  * ---------------------------------------------------------------------------

@@ -32,6 +32,8 @@ SIGNATURES = {
                                        _i64, _i64, _i64, _i32, _i32, _vp, _vp, _size, _vp]),
     "rocs_dca_attention": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32,
                                   _i64, _f32, _i32, _vp, _vp]),
+    "rocs_dca_attention_residual": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32,
+                                           _i32, _i64, _f32, _i32, _vp, _vp, _vp, _vp]),
     "rocs_dca_attention_mapped_workspace_size": (_size, [_i64, _i64]),
     "rocs_dca_attention_mapped": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32,
                                          _i64, _f32, _i32, _vp, _vp, _size, _vp]),
@@ -52,7 +54,7 @@ SIGNATURES = {
     "rocs_validate_offsets": (_i32, [_vp, _i64, _i64, _vp]),
 }
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 NOALLOC_SCRATCH_BYTES = 16 << 20   # ROCS_NOALLOC_SCRATCH_BYTES
 
 

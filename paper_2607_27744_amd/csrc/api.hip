@@ -352,7 +352,8 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
                        const int32_t* kv_offsets, int64_t R, int64_t N, int32_t q_len,
                        int32_t num_heads, int32_t head_dim, int64_t kv_row_stride,
                        float softmax_scale, int32_t dtype, void* out, void* stream,
-                       void* workspace = nullptr, size_t workspace_bytes = 0) {
+                       void* workspace = nullptr, size_t workspace_bytes = 0,
+                       const void* residual = nullptr, void* out_sum = nullptr) {
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (R < 0 || N < 0 || q_len < 1 || num_heads < 1 || head_dim < 1 || kv_row_stride < 0)
     return fail(ROCS_ERR_INVALID_ARGUMENT,
@@ -371,6 +372,8 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
   if (q == nullptr || k == nullptr || v == nullptr || out == nullptr || kv_offsets == nullptr ||
       (mapped ? cand_ids == nullptr : cand_offsets == nullptr))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
+  if ((residual == nullptr) != (out_sum == nullptr))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: residual and out_sum go together", name);
   const size_t es = esize(dtype);
   const size_t out_bytes = (size_t)N * q_len * row_elems * es;
   if (overlap(out, out_bytes, q, out_bytes) || overlap(out, out_bytes, k, 1) ||
@@ -379,6 +382,15 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
       overlap(out, out_bytes, cand_ids, (size_t)N * 4) ||
       overlap(out, out_bytes, kv_offsets, (size_t)(R + 1) * 4))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "out overlaps an input");
+  if (out_sum != nullptr &&
+      (overlap(out_sum, out_bytes, q, out_bytes) || overlap(out_sum, out_bytes, k, 1) ||
+       overlap(out_sum, out_bytes, v, 1) || overlap(out_sum, out_bytes, out, out_bytes) ||
+       overlap(out_sum, out_bytes, residual, out_bytes) ||
+       overlap(out_sum, out_bytes, cand_offsets, (size_t)(R + 1) * 4) ||
+       overlap(out_sum, out_bytes, kv_offsets, (size_t)(R + 1) * 4) ||
+       overlap(out, out_bytes, residual, out_bytes)))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: out_sum overlaps an input or out, or out "
+                "overlaps residual", name);
 
   rocs::AttentionArgs a{};
   a.q = q; a.k = k; a.v = v; a.cand_offsets = cand_offsets; a.kv_offsets = kv_offsets;
@@ -388,9 +400,12 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
   a.bf16 = dtype == ROCS_DTYPE_BF16;
   a.out = out;
   a.ids = mapped ? cand_ids : nullptr;
+  a.residual = residual;
+  a.out_sum = out_sum;
   const bool fast = a.bf16 && (head_dim == 64 || head_dim == 128) && stride % 8 == 0 &&
                     stride < (int64_t(1) << 24) &&
-                    aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16);
+                    aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16) &&
+                    aligned(residual, 16) && aligned(out_sum, 16);
   // Launch limits: a grid may hold fewer than 2^32 work items. The general
   // kernel runs one 64-lane wave per (query row, head) with the rows on the
   // grid's x axis; the tiled kernel runs 256 lanes per (head, tile slot),
@@ -436,6 +451,19 @@ int32_t rocs_dca_attention(const void* q, const void* k, const void* v,
   return attention_impl("rocs_dca_attention", false, q, k, v, cand_offsets, nullptr,
                         kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
                         softmax_scale, dtype, out, stream);
+}
+
+int32_t rocs_dca_attention_residual(const void* q, const void* k, const void* v,
+                                    const int32_t* cand_offsets, const int32_t* kv_offsets,
+                                    int64_t R, int64_t N, int32_t q_len, int32_t num_heads,
+                                    int32_t head_dim, int64_t kv_row_stride,
+                                    float softmax_scale, int32_t dtype, const void* residual,
+                                    void* out, void* out_sum, void* stream) {
+  if (residual == nullptr || out_sum == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "rocs_dca_attention_residual: null residual or out_sum");
+  return attention_impl("rocs_dca_attention_residual", false, q, k, v, cand_offsets, nullptr,
+                        kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
+                        softmax_scale, dtype, out, stream, nullptr, 0, residual, out_sum);
 }
 
 size_t rocs_dca_attention_mapped_workspace_size(int64_t num_requests, int64_t num_cand) {

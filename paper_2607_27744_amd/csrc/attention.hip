@@ -43,6 +43,19 @@ size_t align_up256(size_t n) { return (n + 255) & ~size_t(255); }
 constexpr float kLazyRescale = 64.0f;     // log2 of the largest unnormalised weight
 constexpr float kWeightBound = 0x1p64f;   // per-lane stage sum accepted without a row max
 
+// Eight packed bf16 pairs added elementwise in fp32 and rounded back (RNE).
+__device__ __forceinline__ u32x4 add_bf16x8(u32x4 a, u32x4 b) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float lo = __builtin_bit_cast(float, a[i] << 16) + __builtin_bit_cast(float, b[i] << 16);
+    const float hi = __builtin_bit_cast(float, a[i] & 0xffff0000u) +
+                     __builtin_bit_cast(float, b[i] & 0xffff0000u);
+    r[i] = pack_bf16x2(lo, hi);
+  }
+  return r;
+}
+
 // ---------------------------------------------------------------------------
 // bf16 MFMA kernel (32x32x16 shape), head_dim D in {64, 128}.
 //
@@ -102,7 +115,8 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
-    int64_t slots_per_head, const int32_t* __restrict__ order) {
+    int64_t slots_per_head, const int32_t* __restrict__ order, const bf16_t* __restrict__ res,
+    bf16_t* __restrict__ out_sum) {
   constexpr int NT = 64 * W;
   constexpr int TR = 32 * W;           // query rows per tile
   constexpr int KB = kTileKeys / 32;   // 32-key blocks per stage
@@ -149,12 +163,14 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
     }
   };
   const bf16_t* qh = q + (int64_t)h * D;
-  bf16_t* oh = out + (int64_t)h * D;
 
-  if (L == 0) {                                           // empty history: zeros
+  if (L == 0) {                                  // empty history: zeros (and out_sum = res)
     for (int c = tid; c < rows * (D / 8); c += NT) {
       const int rr = c / (D / 8), dc = (c % (D / 8)) * 8;
-      *reinterpret_cast<u32x4*>(oh + src_row(rr) * qs + dc) = u32x4{0u, 0u, 0u, 0u};
+      const int64_t o = src_row(rr) * qs + (int64_t)h * D + dc;
+      *reinterpret_cast<u32x4*>(out + o) = u32x4{0u, 0u, 0u, 0u};
+      if (res != nullptr)
+        *reinterpret_cast<u32x4*>(out_sum + o) = *reinterpret_cast<const u32x4*>(res + o);
     }
     return;
   }
@@ -435,6 +451,21 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
   const float inv = 1.0f / sum_across_halves(l_part);
   const uint32_t obase = (uint32_t)(wave * 32 * ROWB);
   auto out_swz = [](int row) { return CR == 16 ? (row & 15) : ((row >> 1) & 7); };
+  // Read-back layout: store instruction i covers rows RPS i .. RPS i + RPS - 1
+  // of the wave's 32, lane -> row RPS i + lane / CR, chunk lane % CR. With a
+  // residual, its matching 16-byte pieces are loaded first, so their latency
+  // runs under the LDS round trip and no load waits behind an output store.
+  constexpr int RPS = 1024 / ROWB;            // output rows per store instruction
+  constexpr int NST = 32 / RPS;
+  auto out_off = [&](int i) -> int64_t {
+    const int row = RPS * i + lane_e / CR;
+    return src_row(min(wrow0 + row, rows - 1)) * qs + (int64_t)h * D + 8 * (lane_e % CR);
+  };
+  u32x4 rv[NST];
+  if (res != nullptr) {
+#pragma unroll
+    for (int i = 0; i < NST; ++i) rv[i] = *reinterpret_cast<const u32x4*>(res + out_off(i));
+  }
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -450,14 +481,16 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
       *reinterpret_cast<ROCS_LDS u32x4*>(lds3 + obase + l32e * ROWB + 16 * chunk) =
           u32x4{s0[0], s1[0], s0[1], s1[1]};
     }
-  constexpr int RPS = 1024 / ROWB;            // output rows per store instruction
 #pragma unroll
-  for (int i = 0; i < 32 / RPS; ++i) {
+  for (int i = 0; i < NST; ++i) {
     const int row = RPS * i + lane_e / CR;
     const u32x4 v = *reinterpret_cast<const ROCS_LDS u32x4*>(
         lds3 + obase + row * ROWB + 16 * ((lane_e % CR) ^ out_swz(row)));
-    if (wrow0 + row < rows)
-      *reinterpret_cast<u32x4*>(oh + src_row(wrow0 + row) * qs + 8 * (lane_e % CR)) = v;
+    if (wrow0 + row < rows) {
+      const int64_t o = out_off(i);
+      *reinterpret_cast<u32x4*>(out + o) = v;
+      if (res != nullptr) *reinterpret_cast<u32x4*>(out_sum + o) = add_bf16x8(v, rv[i]);
+    }
   }
 }
 
@@ -471,7 +504,7 @@ __global__ __launch_bounds__(64) void dca_attn_generic(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     T* __restrict__ out, int R, int Tq, int H, int D, int64_t kv_stride, float scale,
-    const int32_t* __restrict__ ids) {
+    const int32_t* __restrict__ ids, const T* __restrict__ res, T* __restrict__ out_sum) {
   const int64_t row = blockIdx.x;
   const int h = blockIdx.y, lane = threadIdx.x;
   // The request: from the caller's per-candidate map (clamped into [0, R),
@@ -515,7 +548,11 @@ __global__ __launch_bounds__(64) void dca_attn_generic(
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int d = lane + 64 * e;
-    if (d < D) out[qo + d] = from_f32<T>(o[e] * inv);
+    if (d < D) {
+      const T y = from_f32<T>(o[e] * inv);
+      out[qo + d] = y;
+      if (res != nullptr) out_sum[qo + d] = from_f32<T>(load_f32(&y) + load_f32(res + qo + d));
+    }
   }
 }
 
@@ -622,7 +659,8 @@ hipError_t launch_fast(const AttentionArgs& a, const int32_t* cand_off, const in
                        static_cast<const bf16_t*>(a.q), static_cast<const bf16_t*>(a.k),
                        static_cast<const bf16_t*>(a.v), cand_off, a.kv_offsets,
                        static_cast<bf16_t*>(a.out), (int)a.R, a.q_len, a.heads, a.kv_stride,
-                       scale_log2, slots, order);
+                       scale_log2, slots, order, static_cast<const bf16_t*>(a.residual),
+                       static_cast<bf16_t*>(a.out_sum));
 }
 
 // The mapped form on the tiled kernel: group, then attend in grouped order.
@@ -655,7 +693,8 @@ hipError_t launch_generic(const AttentionArgs& a, hipStream_t s) {
                        dim3(64), s, static_cast<const T*>(a.q), static_cast<const T*>(a.k),
                        static_cast<const T*>(a.v), a.cand_offsets, a.kv_offsets,
                        static_cast<T*>(a.out), (int)a.R, a.q_len, a.heads, a.head_dim,
-                       a.kv_stride, a.scale, a.ids);
+                       a.kv_stride, a.scale, a.ids, static_cast<const T*>(a.residual),
+                       static_cast<T*>(a.out_sum));
 }
 
 }  // namespace

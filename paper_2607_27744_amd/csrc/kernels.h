@@ -42,6 +42,8 @@ struct AttentionArgs {
   void* out;
   const int32_t* ids;  // caller's per-candidate request map, or NULL (CSR offsets)
   void* workspace;     // grouping workspace of the mapped form (mapped_grouping_bytes), or NULL
+  const void* residual;  // [N, q_len, H, d] added to the rounded output into out_sum, or NULL
+  void* out_sum;
 };
 
 struct InteractionArgs {

@@ -352,6 +352,15 @@ def dca_attention(q, k, v, cand_offsets, kv_offsets, *, scale=None, out=None, st
     return _attention(q, k, v, cand_offsets, None, kv_offsets, scale, out, stream)
 
 
+def dca_attention_residual(q, k, v, cand_offsets, kv_offsets, residual, *, scale=None, out=None,
+                           out_sum=None, stream=None):
+    """dca_attention plus the stacked-DCA residual: returns (out, out_sum) with
+    out_sum = round(out + residual) formed in the kernel's epilogue; residual has
+    q's shape [N, T, H, d]."""
+    return _attention(q, k, v, cand_offsets, None, kv_offsets, scale, out, stream,
+                      residual=residual, out_sum=out_sum)
+
+
 def dca_attention_mapped_workspace_size(num_requests, num_cand):
     return int(_lib.load().rocs_dca_attention_mapped_workspace_size(num_requests, num_cand))
 
@@ -389,7 +398,8 @@ def _identity_offsets(n_req, device):
     return _IDENTITY[key]
 
 
-def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream, workspace=None):
+def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream, workspace=None,
+               residual=None, out_sum=None):
     lib = _lib.load()
     mapped = cand_ids is not None
     _need(q.dim() == 4 and q.is_contiguous(), "q must be a contiguous [N, T, H, d] tensor")
@@ -413,6 +423,19 @@ def _attention(q, k, v, cand_offsets, cand_ids, kv_offsets, scale, out, stream, 
           "out must match q")
     _on_gpu(q, k, v, cand_offsets, cand_ids, kv_offsets, out)
     stride = k.stride(0) if k.shape[0] > 1 else heads * dim
+    if residual is not None:
+        _need(residual.shape == q.shape and residual.dtype == q.dtype and
+              residual.is_contiguous(), "residual must be a contiguous tensor shaped like q")
+        if out_sum is None:
+            out_sum = torch.empty_like(q)
+        _need(out_sum.shape == q.shape and out_sum.dtype == q.dtype and out_sum.is_contiguous(),
+              "out_sum must match q")
+        _on_gpu(residual, out_sum)
+        _lib.check(lib.rocs_dca_attention_residual(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(cand_offsets), _ptr(kv_offsets), n_req, n_cand,
+            q_len, heads, dim, stride, float(scale or 0.0), _dtype_code(q), _ptr(residual),
+            _ptr(out), _ptr(out_sum), _stream(stream)), "rocs_dca_attention_residual")
+        return out, out_sum
     if mapped:
         need = int(lib.rocs_dca_attention_mapped_workspace_size(n_req, n_cand))
         if workspace is None and need > 0:

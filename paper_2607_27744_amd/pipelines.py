@@ -68,6 +68,7 @@ def prepare(w, device="cuda"):
         p.q2 = torch.empty_like(p.q1)
         p.a1 = torch.empty((w.n_cand, 1, h, d), dtype=torch.bfloat16, device=dev)
         p.a2 = torch.empty_like(p.a1)
+        p.u = torch.empty_like(p.a1)      # layer-2 query input, round(A1 + e_c)
         p.h, p.d = h, d
     elif cid == 4:
         # The interaction fused into the linear's operand (rocs_glm_fm_linear):
@@ -103,43 +104,57 @@ def _kv_views(kv, h, d):
     return kv[:, :h * d].view(-1, h, d), kv[:, h * d:].view(-1, h, d)
 
 
+def step_calls(p):
+    """The workload's hot path as its operator calls, in launch order: one
+    zero-argument callable per librocs call (each enqueues on the current
+    stream). `bench.py` times them one by one."""
+    cid = p.config_id
+    n = p.n_cand
+    if cid == 1:
+        return [lambda: ops.ikbo_linear(p.x_cand, p.w_cand, x_req=p.x_req, w_req=p.w_req,
+                                        cand_offsets=p.cand_offsets, activation="relu",
+                                        out=p.linear, workspace=p.ws),
+                lambda: ops.dca_attention(p.q, p.k, p.v, p.cand_offsets, p.kv_offsets,
+                                          out=p.attention)]
+    if cid == 2:
+        return [lambda: ops.ikbo_mlp2(p.x_cand, p.w1_cand, p.w2, x_req=p.x_req,
+                                      w1_req=p.w1_req, cand_offsets=p.cand_offsets,
+                                      activation1="relu", activation2="none", out=p.out,
+                                      workspace=p.ws)]
+    if cid == 3:
+        k1, v1 = _kv_views(p.kv1, p.h, p.d)
+        k2, v2 = _kv_views(p.kv2, p.h, p.d)
+        # The pointwise residual u = A1 + e_c is formed in the layer-1
+        # attention's epilogue, so the layer-2 query projection reads one tensor.
+        return [lambda: ops.ikbo_linear(p.s, p.wkv1, out=p.kv1),
+                lambda: ops.ikbo_linear(p.e_c, p.wq1, out=p.q1),
+                lambda: ops.dca_attention_residual(
+                    p.q1.view(n, 1, p.h, p.d), k1, v1, p.cand_offsets, p.kv_offsets,
+                    p.e_c.view(n, 1, p.h, p.d), out=p.a1, out_sum=p.u),
+                lambda: ops.ikbo_linear(p.s, p.wkv2, out=p.kv2),
+                lambda: ops.ikbo_linear(p.u.view(n, p.h * p.d), p.wq2, out=p.q2),
+                lambda: ops.dca_attention(p.q2.view(n, 1, p.h, p.d), k2, v2, p.cand_offsets,
+                                          p.kv_offsets, out=p.a2)]
+    if cid == 4:
+        return [lambda: ops.glm_fm_linear(p.x_req, p.x_cand, p.cand_offsets, p.w_req,
+                                          p.w_cand, activation="relu", out=p.out,
+                                          workspace=p.ws)]
+    if cid == 5:
+        k, v = _kv_views(p.kv, p.h, p.d)
+        return [lambda: ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
+                                        cand_offsets=p.cand_offsets, activation="relu",
+                                        out=p.h1, workspace=p.ws),
+                lambda: ops.ikbo_linear(p.h1, p.w2, out=p.out2),
+                lambda: ops.ikbo_linear(p.s, p.wkv, out=p.kv),
+                lambda: ops.dca_attention(p.h1.view(n, 1, p.h, p.d), k, v, p.cand_offsets,
+                                          p.kv_offsets, out=p.attention)]
+    raise ValueError(f"unknown workload {cid}")
+
+
 def step(p):
     """One pass of the workload's hot path (enqueue only)."""
-    cid = p.config_id
-    if cid == 1:
-        ops.ikbo_linear(p.x_cand, p.w_cand, x_req=p.x_req, w_req=p.w_req,
-                        cand_offsets=p.cand_offsets, activation="relu", out=p.linear,
-                        workspace=p.ws)
-        ops.dca_attention(p.q, p.k, p.v, p.cand_offsets, p.kv_offsets, out=p.attention)
-    elif cid == 2:
-        ops.ikbo_mlp2(p.x_cand, p.w1_cand, p.w2, x_req=p.x_req, w1_req=p.w1_req,
-                      cand_offsets=p.cand_offsets, activation1="relu", activation2="none",
-                      out=p.out, workspace=p.ws)
-    elif cid == 3:
-        n = p.n_cand
-        ops.ikbo_linear(p.s, p.wkv1, out=p.kv1)
-        ops.ikbo_linear(p.e_c, p.wq1, out=p.q1)
-        k1, v1 = _kv_views(p.kv1, p.h, p.d)
-        ops.dca_attention(p.q1.view(n, 1, p.h, p.d), k1, v1, p.cand_offsets, p.kv_offsets,
-                          out=p.a1)
-        ops.ikbo_linear(p.s, p.wkv2, out=p.kv2)
-        ops.ikbo_linear(p.a1.view(n, p.h * p.d), p.wq2, x_cand_add=p.e_c, out=p.q2)
-        k2, v2 = _kv_views(p.kv2, p.h, p.d)
-        ops.dca_attention(p.q2.view(n, 1, p.h, p.d), k2, v2, p.cand_offsets, p.kv_offsets,
-                          out=p.a2)
-    elif cid == 4:
-        ops.glm_fm_linear(p.x_req, p.x_cand, p.cand_offsets, p.w_req, p.w_cand,
-                          activation="relu", out=p.out, workspace=p.ws)
-    elif cid == 5:
-        n = p.n_cand
-        ops.ikbo_linear(p.x_cand, p.w1_cand, x_req=p.x_req, w_req=p.w1_req,
-                        cand_offsets=p.cand_offsets, activation="relu", out=p.h1,
-                        workspace=p.ws)
-        ops.ikbo_linear(p.h1, p.w2, out=p.out2)
-        ops.ikbo_linear(p.s, p.wkv, out=p.kv)
-        k, v = _kv_views(p.kv, p.h, p.d)
-        ops.dca_attention(p.h1.view(n, 1, p.h, p.d), k, v, p.cand_offsets, p.kv_offsets,
-                          out=p.attention)
+    for call in step_calls(p):
+        call()
     return p
 
 
@@ -148,8 +163,8 @@ def outputs(p):
     return {
         1: lambda: {"linear": p.linear, "attention": p.attention},
         2: lambda: {"out": p.out},
-        3: lambda: {"q1": p.q1, "a1": p.a1.view(p.n_cand, -1), "q2": p.q2,
-                    "a2": p.a2.view(p.n_cand, -1)},
+        3: lambda: {"q1": p.q1, "a1": p.a1.view(p.n_cand, -1), "u": p.u.view(p.n_cand, -1),
+                    "q2": p.q2, "a2": p.a2.view(p.n_cand, -1)},
         4: lambda: {"y_req": p.y_req, "out": p.out},
         5: lambda: {"h1": p.h1, "out2": p.out2, "attention": p.attention.view(p.n_cand, -1)},
     }[p.config_id]()

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 22
+    assert len(names) == 23
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -102,6 +102,24 @@ def test_attention_argument_errors(lib):
     assert call(k=None) == _lib.INVALID_ARGUMENT
     assert call(R=0) == _lib.INVALID_ARGUMENT
     assert call(out=FAKE[0]) == _lib.INVALID_ARGUMENT      # out aliases q
+    assert call(N=0) == _lib.OK
+
+
+@no_gpu
+def test_attention_residual_argument_errors(lib):
+    def call(**kw):
+        a = dict(q=FAKE[0], k=FAKE[1], v=FAKE[2], co=FAKE[3], ko=FAKE[4], R=2, N=4, T=1, H=2,
+                 d=64, stride=0, scale=0.0, dtype=1, res=FAKE[6], out=FAKE[5], out_sum=FAKE[7],
+                 stream=None)
+        a.update(kw)
+        return lib.rocs_dca_attention_residual(*a.values())
+    assert call(res=None) == _lib.INVALID_ARGUMENT
+    assert call(out_sum=None) == _lib.INVALID_ARGUMENT
+    assert call(out_sum=FAKE[5]) == _lib.INVALID_ARGUMENT     # out_sum aliases out
+    assert call(res=FAKE[5]) == _lib.INVALID_ARGUMENT         # out aliases residual
+    assert call(out_sum=FAKE[6]) == _lib.INVALID_ARGUMENT     # out_sum aliases residual
+    assert call(T=0) == _lib.INVALID_ARGUMENT
+    assert call(d=300) == _lib.UNSUPPORTED
     assert call(N=0) == _lib.OK
 
 

@@ -206,3 +206,41 @@ def test_request_side_attention(gpu_lib, head_dim, q_len):
     want = ikbo.dca_attention(case.q, case.k, case.v, np.arange(len(lens) + 1),
                               case.kv_offsets)
     assert_close(got, round_bf16(want), f"request-side d{head_dim} T{q_len}")
+
+
+@pytest.mark.parametrize("shape", SHAPES[:3] + [([5, 40], [0, 70])],
+                         ids=lambda s: f"n{sum(s[0])}-L{sum(s[1])}")
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_attention_residual(gpu_lib, shape, head_dim):
+    # The stacked-DCA residual formed in the epilogue: out is exactly the
+    # plain call's output, out_sum = round(out + residual) in fp32 (RNE), and
+    # an empty history passes the residual through.
+    counts, lens = shape
+    case = wl.attention_case(counts, lens, 2, head_dim, seed=head_dim + 5)
+    rng = np.random.default_rng(head_dim)
+    res = round_bf16(rng.standard_normal(case.q.shape))
+    args = (dev_bf16(case.q), dev_bf16(case.k), dev_bf16(case.v), dev_i32(case.cand_offsets),
+            dev_i32(case.kv_offsets))
+    plain = ops.dca_attention(*args)
+    out, out_sum = ops.dca_attention_residual(*args, dev_bf16(res))
+    torch.cuda.synchronize()
+    assert torch.equal(out, plain)
+    want_sum = (out.float() + dev_bf16(res).float()).to(torch.bfloat16)
+    assert torch.equal(out_sum, want_sum)
+    # Against the oracle: u = round(round(A) + residual).
+    want = round_bf16(ikbo.dca_attention(case.q, case.k, case.v, case.cand_offsets,
+                                         case.kv_offsets))
+    assert_close(host(out_sum), round_bf16(want + res), f"residual {shape} d{head_dim}")
+
+
+def test_attention_residual_general_kernel_fp32(gpu_lib):
+    # fp32 runs the general kernel: out_sum = out + residual exactly.
+    case = wl.attention_case([33, 0, 70], [20, 9, 0], 2, 32, seed=3, bf16=False)
+    res = np.random.default_rng(1).standard_normal(case.q.shape)
+    args = (dev_f32(case.q), dev_f32(case.k), dev_f32(case.v), dev_i32(case.cand_offsets),
+            dev_i32(case.kv_offsets))
+    out, out_sum = ops.dca_attention_residual(*args, dev_f32(res))
+    torch.cuda.synchronize()
+    assert torch.equal(out_sum, out + dev_f32(res))
+    want = ikbo.dca_attention(case.q, case.k, case.v, case.cand_offsets, case.kv_offsets)
+    assert_close(host(out), want, "fp32 attention", atol=1e-4, rtol=1e-4)

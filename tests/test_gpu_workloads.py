@@ -70,7 +70,7 @@ def test_workload3_ranking_dca(gpu_lib):
     rows = tile_rows(w.cand_offsets, 3)
     want = oracle_pipelines.ranking_dca(w, rows=rows)
     _say(f"{rows.size} rows compared")
-    for key in ("q1", "a1", "q2", "a2"):
+    for key in ("q1", "a1", "u", "q2", "a2"):
         assert_close(_rows(got[key], rows), want[key], key)
         assert bool(torch.isfinite(got[key]).all())
 
