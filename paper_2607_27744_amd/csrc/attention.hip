@@ -60,8 +60,9 @@ __device__ __forceinline__ u32x4 add_bf16x8(u32x4 a, u32x4 b) {
 // bf16 MFMA kernel (32x32x16 shape), head_dim D in {64, 128}.
 //
 // Workgroup: 4 waves x 32 query rows = one 128-row tile. With 32 rows a wave
-// needs under 256 VGPRs, and each workgroup's K/V staging fits in 64 KiB of
-// LDS, so two workgroups share a CU: each SIMD runs one wave of each. The two
+// needs under 256 VGPRs (under 168 at head_dim 64), and each workgroup's K/V
+// staging fits in 64 KiB of LDS (32 KiB at head_dim 64), so two workgroups
+// share a CU (three at head_dim 64): each SIMD runs one wave of each. The two
 // waves are not held in step by a common barrier, so one's softmax (VALU)
 // overlaps the other's matrix-core work, and one workgroup's prologue (request
 // lookup, query and first K/V loads) and epilogue run while the other is in
@@ -100,9 +101,12 @@ __device__ __forceinline__ u32x4 add_bf16x8(u32x4 a, u32x4 b) {
 // ---------------------------------------------------------------------------
 template <int D> constexpr int attn_waves() { return 4; }  // query rows / 32 per workgroup
 // Slots per K (and per V) ring: 4 stages in LDS, 64 KiB at head_dim 128, so
-// two workgroups share a CU. (At head_dim 64 a single 4-slot ring holding K
-// and V of a stage together, loaded three stages ahead, measured 5% slower
-// on ranking-sized histories.)
+// two workgroups share a CU; 32 KiB at head_dim 64, where three workgroups
+// share a CU (each wave within 168 registers). (At head_dim 64 a single
+// 4-slot ring holding K and V of a stage together, loaded three stages
+// ahead, measured 5% slower on ranking-sized histories; three-slot K and V
+// rings loaded two steps ahead need runtime slot offsets, spill at 168
+// registers and ran 1.5x slower.)
 constexpr int kRingSlots = 2;
 
 // MAPPED: the candidates arrive grouped by request through a permutation
@@ -111,7 +115,7 @@ constexpr int kRingSlots = 2;
 // rows are gathered and output rows scattered through `order`; everything
 // else is the CSR kernel.
 template <int D, int W, bool MAPPED>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void dca_attn_bf16(
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2))) void dca_attn_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
