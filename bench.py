@@ -91,13 +91,14 @@ def op_plan(w):
         lens = np.diff(np.asarray(w.kv_offsets, dtype=np.int64))
         l_tot = int(lens.sum())
         att = _attention_work(w.n_cand, 1, 4, 64, list(zip(counts, lens)))
-        kv = _linear_work(0, l_tot, 0, 256, 512)
+        # Both layers' K/V projections: one stacked GEMM over the shared S.
+        kv = _linear_work(0, l_tot, 0, 256, 1024)
         q = _linear_work(0, w.n_cand, 0, 256, 256)
         # Layer 1's attention also reads e_c and writes u = round(A1 + e_c).
         att_res = (att[0], att[1] + 2 * 2 * w.n_cand * 256)
-        return [("kv_projection_l1", *kv, "hbm"), ("q_projection_l1", *q, "hbm"),
-                ("dca_attention_l1", *att_res, "hbm"), ("kv_projection_l2", *kv, "hbm"),
-                ("q_projection_l2", *q, "hbm"), ("dca_attention_l2", *att, "hbm")]
+        return [("kv_projection_l1_l2", *kv, "hbm"), ("q_projection_l1", *q, "hbm"),
+                ("dca_attention_l1", *att_res, "hbm"), ("q_projection_l2", *q, "hbm"),
+                ("dca_attention_l2", *att, "hbm")]
     if cid == 4:
         # The interaction feeds the linear's operand on chip: Y^C never reaches HBM.
         ff, _ = _fm_work(w.n_req, w.n_cand, 32, 8, 128)

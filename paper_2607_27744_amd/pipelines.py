@@ -59,11 +59,13 @@ def prepare(w, device="cuda"):
         p.kv_offsets = _i32(w.kv_offsets, dev)
         p.e_c, p.s = _bf16(w.e_c, dev), _bf16(w.s, dev)
         p.wq1, p.wq2 = _bf16(w.wq1, dev), _bf16(w.wq2, dev)
-        p.wkv1 = _bf16(np.concatenate([w.wk1, w.wv1], axis=0), dev)
-        p.wkv2 = _bf16(np.concatenate([w.wk2, w.wv2], axis=0), dev)
+        # Both layers project the same history S (the request-side encoder is
+        # the identity), so their four request-side projections are one
+        # stacked GEMM: [K1 | V1 | K2 | V2] = S [W_k1; W_v1; W_k2; W_v2]^T.
+        p.wkv = _bf16(np.concatenate([w.wk1, w.wv1, w.wk2, w.wv2], axis=0), dev)
         l_tot = w.s.shape[0]
-        p.kv1 = torch.empty((l_tot, 2 * h * d), dtype=torch.bfloat16, device=dev)
-        p.kv2 = torch.empty_like(p.kv1)
+        p.kv = torch.empty((l_tot, 4 * h * d), dtype=torch.bfloat16, device=dev)
+        p.kv1, p.kv2 = p.kv[:, :2 * h * d], p.kv[:, 2 * h * d:]
         p.q1 = torch.empty((w.n_cand, h * d), dtype=torch.bfloat16, device=dev)
         p.q2 = torch.empty_like(p.q1)
         p.a1 = torch.empty((w.n_cand, 1, h, d), dtype=torch.bfloat16, device=dev)
@@ -126,12 +128,11 @@ def step_calls(p):
         k2, v2 = _kv_views(p.kv2, p.h, p.d)
         # The pointwise residual u = A1 + e_c is formed in the layer-1
         # attention's epilogue, so the layer-2 query projection reads one tensor.
-        return [lambda: ops.ikbo_linear(p.s, p.wkv1, out=p.kv1),
+        return [lambda: ops.ikbo_linear(p.s, p.wkv, out=p.kv),
                 lambda: ops.ikbo_linear(p.e_c, p.wq1, out=p.q1),
                 lambda: ops.dca_attention_residual(
                     p.q1.view(n, 1, p.h, p.d), k1, v1, p.cand_offsets, p.kv_offsets,
                     p.e_c.view(n, 1, p.h, p.d), out=p.a1, out_sum=p.u),
-                lambda: ops.ikbo_linear(p.s, p.wkv2, out=p.kv2),
                 lambda: ops.ikbo_linear(p.u.view(n, p.h * p.d), p.wq2, out=p.q2),
                 lambda: ops.dca_attention(p.q2.view(n, 1, p.h, p.d), k2, v2, p.cand_offsets,
                                           p.kv_offsets, out=p.a2)]
