@@ -93,12 +93,14 @@ def op_plan(w):
         att = _attention_work(w.n_cand, 1, 4, 64, list(zip(counts, lens)))
         # Both layers' K/V projections: one stacked GEMM over the shared S.
         kv = _linear_work(0, l_tot, 0, 256, 1024)
-        q = _linear_work(0, w.n_cand, 0, 256, 256)
-        # Layer 1's attention also reads e_c and writes u = round(A1 + e_c).
-        att_res = (att[0], att[1] + 2 * 2 * w.n_cand * 256)
-        return [("kv_projection_l1_l2", *kv, "hbm"), ("q_projection_l1", *q, "hbm"),
-                ("dca_attention_l1", *att_res, "hbm"), ("q_projection_l2", *q, "hbm"),
-                ("dca_attention_l2", *att, "hbm")]
+        # Each attention projects its own queries (x [N, 256] read in place of
+        # Q, plus the 256 x 256 W_q and the projection's flops); layer 1 also
+        # reads e_c as the residual and writes u = round(A1 + e_c).
+        q_flops = 2.0 * w.n_cand * 256 * 256
+        l2 = (att[0] + q_flops, att[1] + 2 * 256 * 256)
+        l1 = (l2[0], l2[1] + 2 * 2 * w.n_cand * 256)
+        return [("kv_projection_l1_l2", *kv, "hbm"), ("dca_attention_proj_l1", *l1, "hbm"),
+                ("dca_attention_proj_l2", *l2, "hbm")]
     if cid == 4:
         # The interaction feeds the linear's operand on chip: Y^C never reaches HBM.
         ff, _ = _fm_work(w.n_req, w.n_cand, 32, 8, 128)

@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define ROCS_ABI_VERSION 3
+#define ROCS_ABI_VERSION 4
 
 typedef enum rocs_status {
   ROCS_OK = 0,
@@ -319,6 +319,43 @@ int32_t rocs_dca_attention_residual(const void* q, const void* k, const void* v,
                                     int64_t kv_row_stride, float softmax_scale, int32_t dtype,
                                     const void* residual, void* out, void* out_sum,
                                     void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_dca_attention_proj: rocs_dca_attention with the candidate queries
+ * projected inside the attention kernel (the candidate side of the DCA query
+ * generator, a linear projection of the candidate's features; Section 3.2,
+ * Eq. dca-query):
+ *
+ *   q[n][t][h][:] = round(x[n][t][:] W_q[h head_dim .. (h + 1) head_dim - 1][:]^T)
+ *
+ * rounded to dtype exactly as a separate projection would store it, then the
+ * attention of rocs_dca_attention over those queries (and, when residual is
+ * given, the out_sum of rocs_dca_attention_residual). The queries never
+ * reach memory.
+ *
+ *   x         [N, q_len, d_in]
+ *   d_in      >= 1
+ *   w_q       [H * head_dim, d_in] (the paper's [out, in] orientation)
+ *   residual  [N, q_len, H, head_dim] or NULL; out_sum likewise (both or
+ *             neither). residual may be x itself when d_in = H * head_dim
+ *             (the stacked-DCA residual of the candidate embedding).
+ * out and out_sum may not overlap x or w_q (ROCS_ERR_INVALID_ARGUMENT); a
+ * NULL w_q is ROCS_ERR_INVALID_ARGUMENT. Every other argument, the result and
+ * the errors are those of rocs_dca_attention. Fast path: its conditions with head_dim 64 and
+ * d_in 256, w_q 16-byte aligned (each workgroup projects its tile's query
+ * rows of one head on the matrix cores, with the operand roles and k order
+ * of the streaming linear, so q matches rocs_ikbo_linear's output bit for
+ * bit). Other shapes and fp32 run the general kernel.
+ * ---------------------------------------------------------------------------
+ */
+int32_t rocs_dca_attention_proj(const void* x, int64_t d_in, const void* w_q,
+                                const void* k, const void* v,
+                                const int32_t* cand_offsets, const int32_t* kv_offsets,
+                                int64_t num_requests, int64_t num_cand,
+                                int32_t q_len, int32_t num_heads, int32_t head_dim,
+                                int64_t kv_row_stride, float softmax_scale, int32_t dtype,
+                                const void* residual, void* out, void* out_sum, void* stream);
 
 /*
  * ---------------------------------------------------------------------------

@@ -353,7 +353,8 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
                        int32_t num_heads, int32_t head_dim, int64_t kv_row_stride,
                        float softmax_scale, int32_t dtype, void* out, void* stream,
                        void* workspace = nullptr, size_t workspace_bytes = 0,
-                       const void* residual = nullptr, void* out_sum = nullptr) {
+                       const void* residual = nullptr, void* out_sum = nullptr,
+                       const void* proj_w = nullptr, int64_t proj_in = 0) {
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (R < 0 || N < 0 || q_len < 1 || num_heads < 1 || head_dim < 1 || kv_row_stride < 0)
     return fail(ROCS_ERR_INVALID_ARGUMENT,
@@ -374,9 +375,16 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
     return fail(ROCS_ERR_INVALID_ARGUMENT, "null pointer argument");
   if ((residual == nullptr) != (out_sum == nullptr))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: residual and out_sum go together", name);
+  if (proj_w != nullptr && (proj_in < 1 || proj_in > kMaxI32))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: need 1 <= d_in < 2^31", name);
   const size_t es = esize(dtype);
   const size_t out_bytes = (size_t)N * q_len * row_elems * es;
-  if (overlap(out, out_bytes, q, out_bytes) || overlap(out, out_bytes, k, 1) ||
+  const size_t q_bytes = proj_w != nullptr ? (size_t)N * q_len * (size_t)proj_in * es : out_bytes;
+  if (proj_w != nullptr && (overlap(out, out_bytes, proj_w, (size_t)row_elems * proj_in * es) ||
+                            overlap(out_sum, out_bytes, proj_w, (size_t)row_elems * proj_in * es) ||
+                            overlap(out_sum, out_bytes, q, q_bytes)))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: an output overlaps x or w_q", name);
+  if (overlap(out, out_bytes, q, q_bytes) || overlap(out, out_bytes, k, 1) ||
       overlap(out, out_bytes, v, 1) ||
       overlap(out, out_bytes, cand_offsets, (size_t)(R + 1) * 4) ||
       overlap(out, out_bytes, cand_ids, (size_t)N * 4) ||
@@ -402,10 +410,12 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
   a.ids = mapped ? cand_ids : nullptr;
   a.residual = residual;
   a.out_sum = out_sum;
+  a.proj_w = proj_w;
+  a.proj_in = (int)proj_in;
   const bool fast = a.bf16 && (head_dim == 64 || head_dim == 128) && stride % 8 == 0 &&
                     stride < (int64_t(1) << 24) &&
                     aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16) &&
-                    aligned(residual, 16) && aligned(out_sum, 16);
+                    aligned(residual, 16) && aligned(out_sum, 16) && aligned(proj_w, 16);
   // Launch limits: a grid may hold fewer than 2^32 work items. The general
   // kernel runs one 64-lane wave per (query row, head) with the rows on the
   // grid's x axis; the tiled kernel runs 256 lanes per (head, tile slot),
@@ -464,6 +474,20 @@ int32_t rocs_dca_attention_residual(const void* q, const void* k, const void* v,
   return attention_impl("rocs_dca_attention_residual", false, q, k, v, cand_offsets, nullptr,
                         kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
                         softmax_scale, dtype, out, stream, nullptr, 0, residual, out_sum);
+}
+
+int32_t rocs_dca_attention_proj(const void* x, int64_t d_in, const void* w_q, const void* k,
+                                const void* v, const int32_t* cand_offsets,
+                                const int32_t* kv_offsets, int64_t R, int64_t N, int32_t q_len,
+                                int32_t num_heads, int32_t head_dim, int64_t kv_row_stride,
+                                float softmax_scale, int32_t dtype, const void* residual,
+                                void* out, void* out_sum, void* stream) {
+  if (w_q == nullptr)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "rocs_dca_attention_proj: null w_q");
+  return attention_impl("rocs_dca_attention_proj", false, x, k, v, cand_offsets, nullptr,
+                        kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
+                        softmax_scale, dtype, out, stream, nullptr, 0, residual, out_sum, w_q,
+                        d_in);
 }
 
 size_t rocs_dca_attention_mapped_workspace_size(int64_t num_requests, int64_t num_cand) {

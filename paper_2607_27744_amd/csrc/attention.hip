@@ -114,13 +114,18 @@ constexpr int kRingSlots = 2;
 // grouped order and grouped position p holds candidate order[p], so query
 // rows are gathered and output rows scattered through `order`; everything
 // else is the CSR kernel.
-template <int D, int W, bool MAPPED>
+// QPROJ: the queries are projected in the prologue (Q = round(X W_q^T), see
+// below) instead of read: `q` is then X [N, T_q, kProjIn] and `wq` is W_q
+// [H D, kProjIn].
+constexpr int kProjIn = 256;   // input width of the fused query projection
+
+template <int D, int W, bool MAPPED, bool QPROJ>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2))) void dca_attn_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
     int64_t slots_per_head, const int32_t* __restrict__ order, const bf16_t* __restrict__ res,
-    bf16_t* __restrict__ out_sum) {
+    bf16_t* __restrict__ out_sum, const bf16_t* __restrict__ wq) {
   constexpr int NT = 64 * W;
   constexpr int TR = 32 * W;           // query rows per tile
   constexpr int KB = kTileKeys / 32;   // 32-key blocks per stage
@@ -184,9 +189,68 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(D == 64 
   const bool active = wrow0 < rows;
   const int qrow = min(wrow0 + l32, rows - 1);            // clamped; extra rows never stored
   bf16x8 qf[KS];
+  if constexpr (!QPROJ) {
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
-    qf[ks] = *reinterpret_cast<const bf16x8*>(qh + src_row(qrow) * qs + 16 * ks + 8 * hh);
+    for (int ks = 0; ks < KS; ++ks)
+      qf[ks] = *reinterpret_cast<const bf16x8*>(qh + src_row(qrow) * qs + 16 * ks + 8 * hh);
+  } else {
+    // The query projection of this head, fused (the candidate side of the
+    // DCA query generator): Q^T = W_q,h X^T on the matrix cores, with the
+    // same operand roles and k order as the streaming GEMM, so Q is
+    // bit-identical to projecting first. W_q,h (D rows of 512 bytes) is
+    // staged in the K/V ring before the ring's first stage; chunk c of row
+    // d sits at position c ^ (d % 16), so the 16 rows read by a quarter-wave
+    // fall on distinct banks. This wave's 32 rows of X are B fragments.
+    static_assert(D == 64 && 2 * kStages * STAGE >= D * kProjIn * 2, "projection staging");
+    constexpr int PK = kProjIn / 16;                      // k-steps (16)
+    constexpr int PRB = kProjIn * 2;                      // bytes of one W_q row (512)
+    constexpr int PNI = D * PRB / 1024 / W;               // DMA loads per wave (8)
+    const char* wsrc = reinterpret_cast<const char*>(wq + (int64_t)h * D * kProjIn);
+    const uint32_t lb = lds_addr(lds);
+#pragma unroll
+    for (int i = 0; i < PNI; ++i) {
+      const int blk = wave * PNI + i;                     // 1 KiB: rows 2 blk, 2 blk + 1
+      const int prow = 2 * blk + (lane >> 5), pos = lane & 31;
+      lds_dma16_sv(wsrc, (uint32_t)(prow * PRB + 16 * (pos ^ (prow & 15))), lb + 1024u * blk);
+    }
+    const bf16_t* xr = q + src_row(qrow) * kProjIn + 8 * hh;
+    bf16x8 xq[PK];
+#pragma unroll
+    for (int s2 = 0; s2 < PK; ++s2) xq[s2] = *reinterpret_cast<const bf16x8*>(xr + 16 * s2);
+    wait_vmcnt<0>();
+    ring_barrier();
+    f32x16 pacc[2];
+#pragma unroll
+    for (int s2 = 0; s2 < PK; ++s2)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const int prow = 32 * b + l32;
+        const bf16x8 a = *reinterpret_cast<const ROCS_LDS bf16x8*>(
+            lds3 + prow * PRB + 16 * ((2 * s2 + hh) ^ (prow & 15)));
+        if (s2 == 0) {
+          const f32x16 zero = {};
+          pacc[b] = mfma32(a, xq[0], zero);
+        } else {
+          pacc[b] = mfma32(a, xq[s2], pacc[b]);
+        }
+      }
+    // Round to bf16 and exchange halves: lane (l32, hh) then holds dims
+    // 32 b + 16 jj + 8 hh .. + 7 of its row, i.e. qf[2 b + jj].
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const f32x16& pa = pacc[b];
+        const uint32_t e0 = pack_bf16x2(pa[8 * jj], pa[8 * jj + 1]);
+        const uint32_t e1 = pack_bf16x2(pa[8 * jj + 2], pa[8 * jj + 3]);
+        const uint32_t o0 = pack_bf16x2(pa[8 * jj + 4], pa[8 * jj + 5]);
+        const uint32_t o1 = pack_bf16x2(pa[8 * jj + 6], pa[8 * jj + 7]);
+        const auto t0 = __builtin_amdgcn_permlane32_swap(e0, o0, false, false);
+        const auto t1 = __builtin_amdgcn_permlane32_swap(e1, o1, false, false);
+        qf[2 * b + jj] = as_bf16x8(u32x4{t0[0], t1[0], t0[1], t1[1]});
+      }
+    ring_barrier();                                       // W_q's LDS goes to the K/V ring
+  }
 
   // DMA staging. Load i of wave w fills LDS rows KPI (NI w + i) .. +KPI-1 of
   // the stage, 16 bytes per lane in lane order: lane -> row KPI (NI w + i) +
@@ -508,7 +572,8 @@ __global__ __launch_bounds__(64) void dca_attn_generic(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     T* __restrict__ out, int R, int Tq, int H, int D, int64_t kv_stride, float scale,
-    const int32_t* __restrict__ ids, const T* __restrict__ res, T* __restrict__ out_sum) {
+    const int32_t* __restrict__ ids, const T* __restrict__ res, T* __restrict__ out_sum,
+    const T* __restrict__ wq, int d_in) {
   const int64_t row = blockIdx.x;
   const int h = blockIdx.y, lane = threadIdx.x;
   // The request: from the caller's per-candidate map (clamped into [0, R),
@@ -523,7 +588,20 @@ __global__ __launch_bounds__(64) void dca_attn_generic(
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const int d = lane + 64 * e;
-    qv[e] = d < D ? load_f32(q + qo + d) : 0.f;
+    if (wq == nullptr) {
+      qv[e] = d < D ? load_f32(q + qo + d) : 0.f;
+    } else if (d < D) {
+      // The fused query projection: q = x W_q^T for this head's dims,
+      // rounded to T as a separate projection would store it.
+      const T* xr = q + row * d_in;
+      const T* wr = wq + ((int64_t)h * D + d) * d_in;
+      float acc = 0.f;
+      for (int kk = 0; kk < d_in; ++kk) acc = fmaf(load_f32(xr + kk), load_f32(wr + kk), acc);
+      const T qt = from_f32<T>(acc);
+      qv[e] = load_f32(&qt);
+    } else {
+      qv[e] = 0.f;
+    }
     o[e] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
@@ -651,7 +729,7 @@ __global__ __launch_bounds__(64) void group_scatter(const int32_t* __restrict__ 
   }
 }
 
-template <int D, bool MAPPED>
+template <int D, bool MAPPED, bool QPROJ = false>
 hipError_t launch_fast(const AttentionArgs& a, const int32_t* cand_off, const int32_t* order,
                        hipStream_t s) {
   constexpr int W = attn_waves<D>(), TR = 32 * W;
@@ -659,12 +737,12 @@ hipError_t launch_fast(const AttentionArgs& a, const int32_t* cand_off, const in
   const int64_t grid = slots * a.heads;
   const float scale_log2 = a.scale * 1.4426950408889634f;
   if (!grid_fits(grid, 64 * W)) return hipErrorInvalidConfiguration;
-  return launch_kernel(dca_attn_bf16<D, W, MAPPED>, dim3((uint32_t)grid), dim3(64 * W), s,
+  return launch_kernel(dca_attn_bf16<D, W, MAPPED, QPROJ>, dim3((uint32_t)grid), dim3(64 * W), s,
                        static_cast<const bf16_t*>(a.q), static_cast<const bf16_t*>(a.k),
                        static_cast<const bf16_t*>(a.v), cand_off, a.kv_offsets,
                        static_cast<bf16_t*>(a.out), (int)a.R, a.q_len, a.heads, a.kv_stride,
                        scale_log2, slots, order, static_cast<const bf16_t*>(a.residual),
-                       static_cast<bf16_t*>(a.out_sum));
+                       static_cast<bf16_t*>(a.out_sum), static_cast<const bf16_t*>(a.proj_w));
 }
 
 // The mapped form on the tiled kernel: group, then attend in grouped order.
@@ -698,7 +776,7 @@ hipError_t launch_generic(const AttentionArgs& a, hipStream_t s) {
                        static_cast<const T*>(a.v), a.cand_offsets, a.kv_offsets,
                        static_cast<T*>(a.out), (int)a.R, a.q_len, a.heads, a.head_dim,
                        a.kv_stride, a.scale, a.ids, static_cast<const T*>(a.residual),
-                       static_cast<T*>(a.out_sum));
+                       static_cast<T*>(a.out_sum), static_cast<const T*>(a.proj_w), a.proj_in);
 }
 
 }  // namespace
@@ -726,6 +804,13 @@ hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s) {
   // The tiled kernel runs on request-contiguous candidates: the CSR offsets,
   // or a caller's per-candidate map grouped by request first (that needs the
   // grouping workspace); otherwise the general kernel runs.
+  if (a.proj_w != nullptr) {
+    // Fused query projection: the tiled kernel for head_dim 64 and a
+    // projection input of kProjIn, the general kernel otherwise.
+    if (fast && a.ids == nullptr && a.head_dim == 64 && a.proj_in == kProjIn)
+      return launch_fast<64, false, true>(a, a.cand_offsets, nullptr, s);
+    return a.bf16 ? launch_generic<bf16_t>(a, s) : launch_generic<float>(a, s);
+  }
   if (fast && a.ids == nullptr)
     return a.head_dim == 128 ? launch_fast<128, false>(a, a.cand_offsets, nullptr, s)
                              : launch_fast<64, false>(a, a.cand_offsets, nullptr, s);

@@ -44,6 +44,8 @@ struct AttentionArgs {
   void* workspace;     // grouping workspace of the mapped form (mapped_grouping_bytes), or NULL
   const void* residual;  // [N, q_len, H, d] added to the rounded output into out_sum, or NULL
   void* out_sum;
+  const void* proj_w;    // W_q [H d, proj_in] when q holds X [N, q_len, proj_in], or NULL
+  int proj_in;
 };
 
 struct InteractionArgs {

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 23
+    assert len(names) == 24
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -119,6 +119,25 @@ def test_attention_residual_argument_errors(lib):
     assert call(res=FAKE[5]) == _lib.INVALID_ARGUMENT         # out aliases residual
     assert call(out_sum=FAKE[6]) == _lib.INVALID_ARGUMENT     # out_sum aliases residual
     assert call(T=0) == _lib.INVALID_ARGUMENT
+    assert call(d=300) == _lib.UNSUPPORTED
+    assert call(N=0) == _lib.OK
+
+
+@no_gpu
+def test_attention_proj_argument_errors(lib):
+    def call(**kw):
+        a = dict(x=FAKE[0], d_in=256, wq=FAKE[8], k=FAKE[1], v=FAKE[2], co=FAKE[3], ko=FAKE[4],
+                 R=2, N=4, T=1, H=2, d=64, stride=0, scale=0.0, dtype=1, res=None, out=FAKE[5],
+                 out_sum=None, stream=None)
+        a.update(kw)
+        return lib.rocs_dca_attention_proj(*a.values())
+    assert call(wq=None) == _lib.INVALID_ARGUMENT
+    assert call(d_in=0) == _lib.INVALID_ARGUMENT
+    assert call(x=None) == _lib.INVALID_ARGUMENT
+    assert call(out=FAKE[0]) == _lib.INVALID_ARGUMENT        # out aliases x
+    assert call(out=FAKE[8]) == _lib.INVALID_ARGUMENT        # out aliases w_q
+    assert call(res=FAKE[6]) == _lib.INVALID_ARGUMENT        # residual without out_sum
+    assert call(res=FAKE[6], out_sum=FAKE[0]) == _lib.INVALID_ARGUMENT   # out_sum aliases x
     assert call(d=300) == _lib.UNSUPPORTED
     assert call(N=0) == _lib.OK
 

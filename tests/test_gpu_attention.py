@@ -244,3 +244,51 @@ def test_attention_residual_general_kernel_fp32(gpu_lib):
     assert torch.equal(out_sum, out + dev_f32(res))
     want = ikbo.dca_attention(case.q, case.k, case.v, case.cand_offsets, case.kv_offsets)
     assert_close(host(out), want, "fp32 attention", atol=1e-4, rtol=1e-4)
+
+
+def _proj_case(counts, lens, heads, dim, d_in, seed, bf16=True, q_len=1):
+    case = wl.attention_case(counts, lens, heads, dim, seed=seed, bf16=bf16, q_len=q_len)
+    rnd = round_bf16 if bf16 else (lambda a: a)
+    x = wl.normal(wl.tensor_rng(seed, 210, 1), (case.n_cand, q_len, d_in), bf16=bf16)
+    wq = wl.normal(wl.tensor_rng(seed, 210, 2), (heads * dim, d_in), std=d_in ** -0.5, bf16=bf16)
+    res = wl.normal(wl.tensor_rng(seed, 210, 3), (case.n_cand, q_len, heads, dim), bf16=bf16)
+    q = ikbo.linear(x.reshape(-1, d_in), wq).reshape(case.n_cand, q_len, heads, dim)
+    want = ikbo.dca_attention(rnd(q), case.k, case.v, case.cand_offsets, case.kv_offsets)
+    return case, x, wq, res, rnd(want)
+
+
+@pytest.mark.parametrize("shape,q_len", [(s, 1) for s in SHAPES[:4]] +
+                         [(([5, 40], [0, 70]), 1), (SHAPES[0], 3)],
+                         ids=lambda s: f"n{sum(s[0])}-L{sum(s[1])}" if isinstance(s, tuple) else f"T{s}")
+def test_attention_proj_matches_project_then_attend(gpu_lib, shape, q_len):
+    # The fused query projection (head_dim 64, d_in 256) uses the streaming
+    # linear's operand roles and k order: out and out_sum equal projecting
+    # with rocs_ikbo_linear and then attending, bit for bit.
+    counts, lens = shape
+    case, x, wq, res, want = _proj_case(counts, lens, 4, 64, 256, seed=21, q_len=q_len)
+    X, WQ, RES = dev_bf16(x), dev_bf16(wq), dev_bf16(res)
+    args = (dev_bf16(case.k), dev_bf16(case.v), dev_i32(case.cand_offsets),
+            dev_i32(case.kv_offsets))
+    q = ops.ikbo_linear(X.view(-1, 256), WQ).view(-1, q_len, 4, 64)
+    ref_out, ref_sum = ops.dca_attention_residual(q, *args, RES)
+    out, out_sum = ops.dca_attention_proj(X, WQ, *args, heads=4, residual=RES)
+    plain = ops.dca_attention_proj(X, WQ, *args, heads=4)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref_out)
+    assert torch.equal(out_sum, ref_sum)
+    assert torch.equal(plain, ref_out)
+    assert_close(host(out), want, f"proj {shape}")
+
+
+@pytest.mark.parametrize("dim,d_in,bf16", [(128, 256, True), (64, 96, True), (32, 48, False)])
+def test_attention_proj_general_kernel(gpu_lib, dim, d_in, bf16):
+    case, x, wq, res, want = _proj_case([33, 0, 70], [20, 9, 100], 2, dim, d_in, seed=dim,
+                                        bf16=bf16)
+    dev = dev_bf16 if bf16 else dev_f32
+    args = (dev(case.k), dev(case.v), dev_i32(case.cand_offsets), dev_i32(case.kv_offsets))
+    out, out_sum = ops.dca_attention_proj(dev(x), dev(wq), *args, heads=2, residual=dev(res))
+    torch.cuda.synchronize()
+    tol = {} if bf16 else dict(atol=1e-4, rtol=1e-4)
+    assert_close(host(out), want, f"proj general d{dim} in{d_in}", **tol)
+    want_sum = (out.float() + dev(res).float()).to(out.dtype)
+    assert torch.equal(out_sum, want_sum)

@@ -70,7 +70,9 @@ def test_workload3_ranking_dca(gpu_lib):
     rows = tile_rows(w.cand_offsets, 3)
     want = oracle_pipelines.ranking_dca(w, rows=rows)
     _say(f"{rows.size} rows compared")
-    for key in ("q1", "a1", "u", "q2", "a2"):
+    # The query projections run inside the attention kernels, so Q1 and Q2
+    # are checked through A1, u and A2.
+    for key in ("a1", "u", "a2"):
         assert_close(_rows(got[key], rows), want[key], key)
         assert bool(torch.isfinite(got[key]).all())
 
