@@ -99,8 +99,10 @@ def op_plan(w):
         q_flops = 2.0 * w.n_cand * 256 * 256
         l2 = (att[0] + q_flops, att[1] + 2 * 256 * 256)
         l1 = (l2[0], l2[1] + 2 * 2 * w.n_cand * 256)
-        return [("kv_projection_l1_l2", *kv, "hbm"), ("dca_attention_proj_l1", *l1, "hbm"),
-                ("dca_attention_proj_l2", *l2, "hbm")]
+        # The tile plan: both offset arrays in, the plan out.
+        plan = (0.0, 4 * (2 * (w.n_req + 1) + 8 + 2 * w.n_req + 1))
+        return [("kv_projection_l1_l2", *kv, "hbm"), ("attention_plan", *plan, "hbm"),
+                ("dca_attention_proj_l1", *l1, "hbm"), ("dca_attention_proj_l2", *l2, "hbm")]
     if cid == 4:
         # The interaction feeds the linear's operand on chip: Y^C never reaches HBM.
         ff, _ = _fm_work(w.n_req, w.n_cand, 32, 8, 128)
@@ -124,8 +126,8 @@ def timed_step_fns(p):
     return pipelines.step_calls(p)
 
 
-_OP_KERNEL = (("dca_attention", "dca_attn_bf16"), ("glm_interaction", "glm_fm_bf16"),
-              ("ikbo_mlp2", "ikbo_mlp2_bf16"), ("glm_fm_linear", "glm_fm_linear_bf16"),
+_OP_KERNEL = (("attention_plan", "attn_plan_kernel"), ("dca_attention", "dca_attn_bf16"),
+              ("glm_interaction", "glm_fm_bf16"), ("ikbo_mlp2", "ikbo_mlp2_bf16"), ("glm_fm_linear", "glm_fm_linear_bf16"),
               ("", "ikbo_gemm_stream"))
 
 

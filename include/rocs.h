@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define ROCS_ABI_VERSION 4
+#define ROCS_ABI_VERSION 5
 
 typedef enum rocs_status {
   ROCS_OK = 0,
@@ -322,40 +322,78 @@ int32_t rocs_dca_attention_residual(const void* q, const void* k, const void* v,
 
 /*
  * ---------------------------------------------------------------------------
- * rocs_dca_attention_proj: rocs_dca_attention with the candidate queries
- * projected inside the attention kernel (the candidate side of the DCA query
- * generator, a linear projection of the candidate's features; Section 3.2,
- * Eq. dca-query):
+ * rocs_dca_attention_ex: rocs_dca_attention with three options, any
+ * combination of them:
  *
- *   q[n][t][h][:] = round(x[n][t][:] W_q[h head_dim .. (h + 1) head_dim - 1][:]^T)
+ * - fused query projection (w_q non-NULL): the candidate queries are the
+ *   candidate side of the DCA query generator, a linear projection of the
+ *   candidate's features (Section 3.2, Eq. dca-query), computed inside the
+ *   attention kernel:
  *
- * rounded to dtype exactly as a separate projection would store it, then the
- * attention of rocs_dca_attention over those queries (and, when residual is
- * given, the out_sum of rocs_dca_attention_residual). The queries never
- * reach memory.
+ *     q[n][t][h][:] = round(x[n][t][:] W_q[h head_dim .. (h + 1) head_dim - 1][:]^T)
  *
- *   x         [N, q_len, d_in]
- *   d_in      >= 1
- *   w_q       [H * head_dim, d_in] (the paper's [out, in] orientation)
- *   residual  [N, q_len, H, head_dim] or NULL; out_sum likewise (both or
- *             neither). residual may be x itself when d_in = H * head_dim
- *             (the stacked-DCA residual of the candidate embedding).
- * out and out_sum may not overlap x or w_q (ROCS_ERR_INVALID_ARGUMENT); a
- * NULL w_q is ROCS_ERR_INVALID_ARGUMENT. Every other argument, the result and
- * the errors are those of rocs_dca_attention. Fast path: its conditions with head_dim 64 and
- * d_in 256, w_q 16-byte aligned (each workgroup projects its tile's query
- * rows of one head on the matrix cores, with the operand roles and k order
- * of the streaming linear, so q matches rocs_ikbo_linear's output bit for
- * bit). Other shapes and fp32 run the general kernel.
+ *   rounded to dtype exactly as a separate projection would store it; the
+ *   queries never reach memory. `q` then holds x [N, q_len, d_in] (d_in >= 1)
+ *   and w_q is [H * head_dim, d_in] (the paper's [out, in] orientation).
+ *   With w_q NULL, q is the query [N, q_len, H, head_dim] and d_in is
+ *   ignored.
+ * - residual (non-NULL, with out_sum): out_sum = round(out + residual), as
+ *   rocs_dca_attention_residual. residual may be x itself when d_in =
+ *   H * head_dim (the stacked-DCA residual of the candidate embedding).
+ * - plan (non-NULL): the tile order made by rocs_dca_attention_plan for
+ *   these cand_offsets and kv_offsets, R, q_len and num_heads; plan_bytes >=
+ *   rocs_dca_attention_plan_size(R) (else ROCS_ERR_WORKSPACE_TOO_SMALL),
+ *   4-byte aligned, read only. The tiled kernel then takes its 128-row tiles
+ *   longest history first. Results are bit-identical with or without it. A
+ *   plan made for another R, q_len or num_heads is ignored (the built-in
+ *   order runs); one made for other offsets of the same R gives wrong rows
+ *   but never an access outside the arguments.
+ *
+ * out, out_sum and plan may not overlap x, w_q or each other
+ * (ROCS_ERR_INVALID_ARGUMENT). Every other argument, the result and the
+ * errors are those of rocs_dca_attention. Fast path: its conditions (with
+ * the projection: head_dim 64, d_in 256 and w_q 16-byte aligned; each
+ * workgroup projects its tile's query rows of one head on the matrix cores,
+ * with the operand roles and k order of the streaming linear, so q matches
+ * rocs_ikbo_linear's output bit for bit). Other shapes and fp32 run the
+ * general kernel, which ignores the plan.
  * ---------------------------------------------------------------------------
  */
-int32_t rocs_dca_attention_proj(const void* x, int64_t d_in, const void* w_q,
-                                const void* k, const void* v,
-                                const int32_t* cand_offsets, const int32_t* kv_offsets,
-                                int64_t num_requests, int64_t num_cand,
-                                int32_t q_len, int32_t num_heads, int32_t head_dim,
-                                int64_t kv_row_stride, float softmax_scale, int32_t dtype,
-                                const void* residual, void* out, void* out_sum, void* stream);
+int32_t rocs_dca_attention_ex(const void* q, int64_t d_in, const void* w_q, const void* k,
+                              const void* v, const int32_t* cand_offsets,
+                              const int32_t* kv_offsets, const void* plan, size_t plan_bytes,
+                              int64_t num_requests, int64_t num_cand, int32_t q_len,
+                              int32_t num_heads, int32_t head_dim, int64_t kv_row_stride,
+                              float softmax_scale, int32_t dtype, const void* residual,
+                              void* out, void* out_sum, void* stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * rocs_dca_attention_plan: the tile order of the tiled DCA kernel for one
+ * batch (Section 4.3: candidates of one request share its K/V; the kernel's
+ * time per tile grows with the request's history length). Written on
+ * `stream` into plan (device memory, plan_bytes >=
+ * rocs_dca_attention_plan_size(R), 4-byte aligned), from the device offsets
+ * cand_offsets [R + 1] and kv_offsets [R + 1] (valid CSR offsets, as for
+ * rocs_dca_attention), for q_len query tokens per candidate and num_heads
+ * heads. Longest history first (histories of 2^20 - 1 rows or more count
+ * as equal), ties by request index; all heads of one request next to each
+ * other. Up to 4096 requests; beyond that the plan
+ * records the kernel's built-in order. One plan serves every attention call
+ * over the same offsets, q_len and num_heads (e.g. all DCA layers of a
+ * batch). Errors: negative sizes, q_len or num_heads < 1, NULL pointers
+ * (ROCS_ERR_INVALID_ARGUMENT); too small a plan (ROCS_ERR_WORKSPACE_TOO_SMALL);
+ * (R + ceil(N q_len / 128)) num_heads >= 2^24 (ROCS_ERR_UNSUPPORTED).
+ *
+ * rocs_dca_attention_plan_size: bytes of the plan for R requests (0 for a
+ * negative R or R >= 2^31).
+ * ---------------------------------------------------------------------------
+ */
+size_t rocs_dca_attention_plan_size(int64_t num_requests);
+int32_t rocs_dca_attention_plan(const int32_t* cand_offsets, const int32_t* kv_offsets,
+                                int64_t num_requests, int64_t num_cand, int32_t q_len,
+                                int32_t num_heads, void* plan, size_t plan_bytes,
+                                void* stream);
 
 /*
  * ---------------------------------------------------------------------------

@@ -34,8 +34,11 @@ SIGNATURES = {
                                   _i64, _f32, _i32, _vp, _vp]),
     "rocs_dca_attention_residual": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32,
                                            _i32, _i64, _f32, _i32, _vp, _vp, _vp, _vp]),
-    "rocs_dca_attention_proj": (_i32, [_vp, _i64, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32,
-                                       _i32, _i32, _i64, _f32, _i32, _vp, _vp, _vp, _vp]),
+    "rocs_dca_attention_ex": (_i32, [_vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _size, _i64,
+                                     _i64, _i32, _i32, _i32, _i64, _f32, _i32, _vp, _vp, _vp,
+                                     _vp]),
+    "rocs_dca_attention_plan_size": (_size, [_i64]),
+    "rocs_dca_attention_plan": (_i32, [_vp, _vp, _i64, _i64, _i32, _i32, _vp, _size, _vp]),
     "rocs_dca_attention_mapped_workspace_size": (_size, [_i64, _i64]),
     "rocs_dca_attention_mapped": (_i32, [_vp, _vp, _vp, _vp, _vp, _i64, _i64, _i32, _i32, _i32,
                                          _i64, _f32, _i32, _vp, _vp, _size, _vp]),
@@ -56,7 +59,7 @@ SIGNATURES = {
     "rocs_validate_offsets": (_i32, [_vp, _i64, _i64, _vp]),
 }
 
-ABI_VERSION = 4
+ABI_VERSION = 5
 NOALLOC_SCRATCH_BYTES = 16 << 20   # ROCS_NOALLOC_SCRATCH_BYTES
 
 

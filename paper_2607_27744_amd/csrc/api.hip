@@ -354,7 +354,8 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
                        float softmax_scale, int32_t dtype, void* out, void* stream,
                        void* workspace = nullptr, size_t workspace_bytes = 0,
                        const void* residual = nullptr, void* out_sum = nullptr,
-                       const void* proj_w = nullptr, int64_t proj_in = 0) {
+                       const void* proj_w = nullptr, int64_t proj_in = 0,
+                       const void* plan = nullptr, size_t plan_bytes = 0) {
   if (!valid_dtype(dtype)) return fail(ROCS_ERR_INVALID_ARGUMENT, "unknown dtype %d", dtype);
   if (R < 0 || N < 0 || q_len < 1 || num_heads < 1 || head_dim < 1 || kv_row_stride < 0)
     return fail(ROCS_ERR_INVALID_ARGUMENT,
@@ -399,6 +400,15 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
        overlap(out, out_bytes, residual, out_bytes)))
     return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: out_sum overlaps an input or out, or out "
                 "overlaps residual", name);
+  if (plan != nullptr) {
+    if (plan_bytes < rocs::attention_plan_bytes(R))
+      return fail(ROCS_ERR_WORKSPACE_TOO_SMALL, "%s: plan needs %zu bytes, got %zu", name,
+                  rocs::attention_plan_bytes(R), plan_bytes);
+    if (!aligned(plan, 4) || overlap(out, out_bytes, plan, plan_bytes) ||
+        overlap(out_sum, out_bytes, plan, plan_bytes))
+      return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: plan misaligned or overlapping an output",
+                  name);
+  }
 
   rocs::AttentionArgs a{};
   a.q = q; a.k = k; a.v = v; a.cand_offsets = cand_offsets; a.kv_offsets = kv_offsets;
@@ -412,6 +422,7 @@ int32_t attention_impl(const char* name, bool mapped, const void* q, const void*
   a.out_sum = out_sum;
   a.proj_w = proj_w;
   a.proj_in = (int)proj_in;
+  a.plan = static_cast<const int32_t*>(plan);
   const bool fast = a.bf16 && (head_dim == 64 || head_dim == 128) && stride % 8 == 0 &&
                     stride < (int64_t(1) << 24) &&
                     aligned(q, 16) && aligned(k, 16) && aligned(v, 16) && aligned(out, 16) &&
@@ -476,18 +487,50 @@ int32_t rocs_dca_attention_residual(const void* q, const void* k, const void* v,
                         softmax_scale, dtype, out, stream, nullptr, 0, residual, out_sum);
 }
 
-int32_t rocs_dca_attention_proj(const void* x, int64_t d_in, const void* w_q, const void* k,
-                                const void* v, const int32_t* cand_offsets,
-                                const int32_t* kv_offsets, int64_t R, int64_t N, int32_t q_len,
-                                int32_t num_heads, int32_t head_dim, int64_t kv_row_stride,
-                                float softmax_scale, int32_t dtype, const void* residual,
-                                void* out, void* out_sum, void* stream) {
-  if (w_q == nullptr)
-    return fail(ROCS_ERR_INVALID_ARGUMENT, "rocs_dca_attention_proj: null w_q");
-  return attention_impl("rocs_dca_attention_proj", false, x, k, v, cand_offsets, nullptr,
+int32_t rocs_dca_attention_ex(const void* q, int64_t d_in, const void* w_q, const void* k,
+                              const void* v, const int32_t* cand_offsets,
+                              const int32_t* kv_offsets, const void* plan, size_t plan_bytes,
+                              int64_t R, int64_t N, int32_t q_len, int32_t num_heads,
+                              int32_t head_dim, int64_t kv_row_stride, float softmax_scale,
+                              int32_t dtype, const void* residual, void* out, void* out_sum,
+                              void* stream) {
+  return attention_impl("rocs_dca_attention_ex", false, q, k, v, cand_offsets, nullptr,
                         kv_offsets, R, N, q_len, num_heads, head_dim, kv_row_stride,
                         softmax_scale, dtype, out, stream, nullptr, 0, residual, out_sum, w_q,
-                        d_in);
+                        w_q != nullptr ? d_in : 0, plan, plan_bytes);
+}
+
+size_t rocs_dca_attention_plan_size(int64_t num_requests) {
+  if (num_requests < 0 || num_requests > kMaxI32) return 0;
+  return rocs::attention_plan_bytes(num_requests);
+}
+
+int32_t rocs_dca_attention_plan(const int32_t* cand_offsets, const int32_t* kv_offsets,
+                                int64_t R, int64_t N, int32_t q_len, int32_t num_heads,
+                                void* plan, size_t plan_bytes, void* stream) {
+  static const char* name = "rocs_dca_attention_plan";
+  if (R < 0 || N < 0 || q_len < 1 || num_heads < 1)
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: need R >= 0, N >= 0, q_len >= 1, "
+                "num_heads >= 1", name);
+  if (R > kMaxI32 || N * q_len > kMaxI32 || num_heads > 65535 ||
+      (R + (N * q_len + 127) / 128) * num_heads >= (int64_t(1) << 24))
+    return fail(ROCS_ERR_UNSUPPORTED, "%s: (R + N * q_len / 128) * num_heads tiles exceed the "
+                "tiled kernel's grid limit (2^24)", name);
+  if (plan == nullptr || (R > 0 && (cand_offsets == nullptr || kv_offsets == nullptr)))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: null pointer argument", name);
+  if (plan_bytes < rocs::attention_plan_bytes(R))
+    return fail(ROCS_ERR_WORKSPACE_TOO_SMALL, "%s: plan needs %zu bytes, got %zu", name,
+                rocs::attention_plan_bytes(R), plan_bytes);
+  if (!aligned(plan, 4))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: plan must be 4-byte aligned", name);
+  if (overlap(plan, plan_bytes, cand_offsets, (size_t)(R + 1) * 4) ||
+      overlap(plan, plan_bytes, kv_offsets, (size_t)(R + 1) * 4))
+    return fail(ROCS_ERR_INVALID_ARGUMENT, "%s: plan overlaps the offsets", name);
+  const hipError_t e = rocs::launch_attention_plan(cand_offsets, kv_offsets, R, q_len,
+                                                   num_heads, static_cast<int32_t*>(plan),
+                                                   static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return launch_failed(name, e);
+  return ok();
 }
 
 size_t rocs_dca_attention_mapped_workspace_size(int64_t num_requests, int64_t num_cand) {

@@ -119,15 +119,48 @@ constexpr int kRingSlots = 2;
 // [H D, kProjIn].
 constexpr int kProjIn = 256;   // input width of the fused query projection
 
+// Tile plan (launch_attention_plan): an int32 array. Header: mode (1 =
+// sorted, 0 = use the built-in order), T (tiles over all heads), R, H, T_q,
+// rows per tile; then from kPlanHeader the request ids sorted by history
+// length, longest first (ties by id), and their tile offsets P[0..R]
+// (P[i+1] - P[i] = H * ceil(n_r T_q / rows per tile) for the i-th request r;
+// all heads of one request are consecutive, each head's tiles in order).
+// Workgroup b takes tile t of that list, in chunks of kPlanChunk consecutive
+// tiles per XCD: t = ((b / 8) / C * 8 + b % 8) C + (b / 8) % C, so the chunks
+// of the longest histories are spread over all XCDs first and a chunk (a
+// request's tiles, sharing its K/V) stays on one L2.
+constexpr int kPlanHeader = 8;
+constexpr int kPlanChunk = 16;
+constexpr int kAttnTileRows = 128;   // query rows per tile (4 waves x 32) at head_dim 64 and 128
+
+// Largest g in [0, n) with P[g] <= t, given P[0] <= t and P non-decreasing;
+// wave-parallel like request_of_slot. Call with every lane of the wave active.
+__device__ __forceinline__ int plan_group_of(const int32_t* __restrict__ P, int n, int64_t t) {
+  const int lane = (int)(threadIdx.x & 63);
+  int lo = 0;
+  while (n > 1) {
+    const int step = (n + 63) / 64;
+    const int g = lo + lane * step;
+    const bool ok = g < lo + n && (int64_t)P[g] <= t;
+    const uint64_t m = __ballot(ok);
+    const int k = 63 - __builtin_clzll(m);
+    lo += k * step;
+    n = min(step, n - k * step);
+  }
+  return __builtin_amdgcn_readfirstlane(lo);
+}
+
 template <int D, int W, bool MAPPED, bool QPROJ>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 2))) void dca_attn_bf16(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off,
     bf16_t* __restrict__ out, int R, int Tq, int H, int64_t kv_stride, float scale_log2,
     int64_t slots_per_head, const int32_t* __restrict__ order, const bf16_t* __restrict__ res,
-    bf16_t* __restrict__ out_sum, const bf16_t* __restrict__ wq) {
+    bf16_t* __restrict__ out_sum, const bf16_t* __restrict__ wq,
+    const int32_t* __restrict__ plan) {
   constexpr int NT = 64 * W;
   constexpr int TR = 32 * W;           // query rows per tile
+  static_assert(TR == kAttnTileRows, "the tile plan assumes 128-row tiles");
   constexpr int KB = kTileKeys / 32;   // 32-key blocks per stage
   constexpr int KS = D / 16;           // MFMA steps over head_dim
   constexpr int DB = D / 32;           // 32-wide output column blocks
@@ -147,11 +180,40 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(D == 64 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  const uint32_t work = xcd_remap(blockIdx.x, gridDim.x);
-  const int h = (int)(work / (uint64_t)slots_per_head);
-  const int64_t slot = (int64_t)(work % (uint64_t)slots_per_head);
-  const int r = request_of_slot(cand_off, R, slot, Tq, TR);
-  const int64_t j = slot - tile_base(cand_off, r, Tq, TR);
+  // This workgroup's (head, request, tile of the request): from the
+  // caller's plan when it matches this launch, else the built-in order
+  // (head-major slots R + ceil(N T_q / TR) per head, XCD-remapped). The
+  // planned grid is rounded up to whole chunk rounds; surplus workgroups
+  // exit. A plan never moves an access out of range: its request ids are
+  // clamped and a tile past its request's rows is idle.
+  int h, r;
+  int64_t j;
+  const uint32_t b = blockIdx.x;
+  const int64_t n_work = slots_per_head * H;
+  if (plan != nullptr && plan[0] == 1 && plan[2] == R && plan[3] == H && plan[4] == Tq &&
+      plan[5] == TR) {
+    const uint32_t xi = b / kNumXcd;
+    const int64_t t = ((int64_t)(xi / kPlanChunk) * kNumXcd + b % kNumXcd) * kPlanChunk +
+                      xi % kPlanChunk;
+    if (t >= plan[1]) return;
+    const int32_t* P = plan + kPlanHeader + R;
+    const int g = plan_group_of(P, R, t);
+    r = (int)min((uint32_t)plan[kPlanHeader + g], (uint32_t)(R - 1));
+    const int p0 = P[g];
+    const int per_head = (P[g + 1] - p0) / H;
+    if (per_head < 1) return;
+    const int off = (int)(t - p0);
+    h = off / per_head;
+    j = off - (int64_t)h * per_head;
+    if (h >= H) return;
+  } else {
+    if ((int64_t)b >= n_work) return;
+    const uint32_t work = xcd_remap(b, (uint32_t)n_work);
+    h = (int)(work / (uint64_t)slots_per_head);
+    const int64_t slot = (int64_t)(work % (uint64_t)slots_per_head);
+    r = request_of_slot(cand_off, R, slot, Tq, TR);
+    j = slot - tile_base(cand_off, r, Tq, TR);
+  }
   const int64_t rend = (int64_t)cand_off[r + 1] * Tq;
   const int64_t row0 = (int64_t)cand_off[r] * Tq + j * TR;
   if (row0 >= rend) return;                               // idle slot
@@ -729,12 +791,170 @@ __global__ __launch_bounds__(64) void group_scatter(const int32_t* __restrict__ 
   }
 }
 
+// ---------------------------------------------------------------------------
+// Tile plan for one batch (one workgroup of 256 threads, one wave per SIMD):
+// every request's history length and tile count are read in one pass; the
+// requests are sorted by (history length descending, index) as 32-bit keys
+// in LDS (kPlanLenBits bits of clamped length, 12 bits of index): up to 256
+// requests by counting each key's rank, more with a bitonic sort; an
+// exclusive scan of the tile counts in that order gives P. Beyond
+// kAttnPlanMaxSort requests only the header is written (mode 0: the kernel
+// keeps its built-in order).
+// ---------------------------------------------------------------------------
+constexpr int kPlanThreads = 256;
+constexpr int kPlanIdBits = 12;
+constexpr int kPlanLenBits = 32 - kPlanIdBits;   // lengths beyond 2^20 - 1 tie
+static_assert(kAttnPlanMaxSort == (1 << kPlanIdBits), "plan key layout");
+
+__global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(
+    const int32_t* __restrict__ cand_off, const int32_t* __restrict__ kv_off, int R, int Tq,
+    int H, int32_t* __restrict__ plan) {
+  constexpr int PER = (int)kAttnPlanMaxSort / kPlanThreads;   // sorted positions per thread
+  constexpr uint32_t kLenMax = (1u << kPlanLenBits) - 1;
+  __shared__ __attribute__((aligned(16))) uint32_t key[kAttnPlanMaxSort];
+  __shared__ int32_t tiles[kAttnPlanMaxSort];
+  __shared__ int32_t wsum[kPlanThreads / 64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (R > kAttnPlanMaxSort) {
+    if (tid < kPlanHeader) plan[tid] = tid == 2 ? R : 0;   // mode 0
+    return;
+  }
+  int32_t* ids = plan + kPlanHeader;
+  int32_t* P = ids + R;
+  if (R <= kPlanThreads) {
+    // Up to one request per thread: its sorted position is the number of
+    // smaller keys (keys are distinct), counted over the LDS copy four keys
+    // per read; then the tile counts are scanned in sorted order.
+    uint32_t kk = ~0u;
+    int tl = 0;
+    if (tid < R) {
+      const uint32_t L = (uint32_t)max(kv_off[tid + 1] - kv_off[tid], 0);
+      const int64_t rows = (int64_t)max(cand_off[tid + 1] - cand_off[tid], 0) * Tq;
+      kk = ((kLenMax - min(L, kLenMax)) << kPlanIdBits) | (uint32_t)tid;
+      tl = (int)((rows + kAttnTileRows - 1) / kAttnTileRows) * H;
+    }
+    key[tid] = kk;                                         // padding: ~0, never smaller
+    __syncthreads();
+    int rank = 0;
+    const uint4* k4 = reinterpret_cast<const uint4*>(key);
+#pragma unroll 8
+    for (int c = 0; c < kPlanThreads / 4; ++c) {
+      const uint4 q = k4[c];
+      rank += (q.x < kk) + (q.y < kk) + (q.z < kk) + (q.w < kk);
+    }
+    if (tid < R) {
+      tiles[rank] = tl;
+      ids[rank] = tid;
+    }
+    __syncthreads();
+    const int t = tid < R ? tiles[tid] : 0;
+    int incl = t;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o);
+      if (lane >= o) incl += y;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    int run = incl - t;
+    for (int w = 0; w < wave; ++w) run += wsum[w];
+    if (tid < R) P[tid] = run;
+    if (tid == R - 1) {
+      P[R] = run + t;
+      plan[1] = run + t;
+    }
+    if (tid == 0) {
+      if (R == 0) {
+        P[0] = 0;
+        plan[1] = 0;
+      }
+      plan[0] = 1;
+      plan[2] = R;
+      plan[3] = H;
+      plan[4] = Tq;
+      plan[5] = kAttnTileRows;
+      plan[6] = 0;
+      plan[7] = 0;
+    }
+    return;
+  }
+  int n = 1;
+  while (n < R) n <<= 1;
+  for (int i = tid; i < n; i += kPlanThreads) {
+    uint32_t kk = ~0u;                                     // padding sorts last
+    if (i < R) {
+      const uint32_t L = (uint32_t)max(kv_off[i + 1] - kv_off[i], 0);
+      const int64_t rows = (int64_t)max(cand_off[i + 1] - cand_off[i], 0) * Tq;
+      kk = ((kLenMax - min(L, kLenMax)) << kPlanIdBits) | (uint32_t)i;
+      tiles[i] = (int)((rows + kAttnTileRows - 1) / kAttnTileRows) * H;
+    }
+    key[i] = kk;
+  }
+  __syncthreads();
+  for (int size = 2; size <= n; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      for (int i = tid; i < n / 2; i += kPlanThreads) {
+        const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+        const uint32_t x = key[lo], y = key[hi];
+        if ((x > y) == ((lo & size) == 0)) {
+          key[lo] = y;
+          key[hi] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // Thread tid owns sorted positions PER tid .. PER tid + PER - 1.
+  int cnt[PER], rid[PER], tsum = 0;
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int i = PER * tid + e;
+    rid[e] = i < R ? (int)(key[i] & ((1u << kPlanIdBits) - 1)) : 0;
+    cnt[e] = i < R ? tiles[rid[e]] : 0;
+    tsum += cnt[e];
+  }
+  // Block exclusive scan of the per-thread sums.
+  int incl = tsum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o);
+    if (lane >= o) incl += y;
+  }
+  if (lane == 63) wsum[wave] = incl;
+  __syncthreads();
+  int run = incl - tsum;
+  for (int w = 0; w < wave; ++w) run += wsum[w];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) {
+    const int i = PER * tid + e;
+    if (i < R) {
+      ids[i] = rid[e];
+      P[i] = run;
+    }
+    run += cnt[e];
+  }
+  if (tid == kPlanThreads - 1) {
+    P[R] = run;
+    plan[0] = 1;
+    plan[1] = run;
+    plan[2] = R;
+    plan[3] = H;
+    plan[4] = Tq;
+    plan[5] = kAttnTileRows;
+    plan[6] = 0;
+    plan[7] = 0;
+  }
+}
+
 template <int D, bool MAPPED, bool QPROJ = false>
 hipError_t launch_fast(const AttentionArgs& a, const int32_t* cand_off, const int32_t* order,
                        hipStream_t s) {
   constexpr int W = attn_waves<D>(), TR = 32 * W;
   const int64_t slots = a.R + (a.N * a.q_len + TR - 1) / TR;
-  const int64_t grid = slots * a.heads;
+  constexpr int64_t kRound = (int64_t)kNumXcd * kPlanChunk;
+  const int32_t* plan = MAPPED ? nullptr : a.plan;
+  const int64_t grid = plan != nullptr ? (slots * a.heads + kRound - 1) / kRound * kRound
+                                       : slots * a.heads;
   const float scale_log2 = a.scale * 1.4426950408889634f;
   if (!grid_fits(grid, 64 * W)) return hipErrorInvalidConfiguration;
   return launch_kernel(dca_attn_bf16<D, W, MAPPED, QPROJ>, dim3((uint32_t)grid), dim3(64 * W), s,
@@ -742,7 +962,8 @@ hipError_t launch_fast(const AttentionArgs& a, const int32_t* cand_off, const in
                        static_cast<const bf16_t*>(a.v), cand_off, a.kv_offsets,
                        static_cast<bf16_t*>(a.out), (int)a.R, a.q_len, a.heads, a.kv_stride,
                        scale_log2, slots, order, static_cast<const bf16_t*>(a.residual),
-                       static_cast<bf16_t*>(a.out_sum), static_cast<const bf16_t*>(a.proj_w));
+                       static_cast<bf16_t*>(a.out_sum), static_cast<const bf16_t*>(a.proj_w),
+                       plan);
 }
 
 // The mapped form on the tiled kernel: group, then attend in grouped order.
@@ -798,6 +1019,16 @@ size_t mapped_grouping_bytes(int64_t R, int64_t N) {
   if (!mapped_grouping_plan(R, N, &G, &nb)) return 0;
   return align_up256((size_t)(R + 1) * 4) + align_up256((size_t)N * 4) +
          align_up256((size_t)R * (size_t)nb * 4);
+}
+
+size_t attention_plan_bytes(int64_t R) {
+  return align_up256((size_t)(kPlanHeader + 2 * R + 1) * sizeof(int32_t));
+}
+
+hipError_t launch_attention_plan(const int32_t* cand_off, const int32_t* kv_off, int64_t R,
+                                 int q_len, int heads, int32_t* plan, hipStream_t s) {
+  return launch_kernel(attn_plan_kernel, dim3(1), dim3(kPlanThreads), s, cand_off, kv_off,
+                       (int)R, q_len, heads, plan);
 }
 
 hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s) {

@@ -46,6 +46,7 @@ struct AttentionArgs {
   void* out_sum;
   const void* proj_w;    // W_q [H d, proj_in] when q holds X [N, q_len, proj_in], or NULL
   int proj_in;
+  const int32_t* plan;   // tile order from launch_attention_plan (attention_plan_bytes(R)), or NULL
 };
 
 struct InteractionArgs {
@@ -116,6 +117,13 @@ hipError_t launch_request_ids(const int32_t* off, int64_t R, int64_t N, int32_t*
                               hipStream_t s);
 hipError_t launch_linear(const LinearArgs& a, bool fast, hipStream_t s);
 hipError_t launch_attention(const AttentionArgs& a, bool fast, hipStream_t s);
+// Tile order of the tiled attention kernel for one batch's offsets: longest
+// history first (requests up to kAttnPlanMaxSort; beyond that the plan says
+// "built-in order"). Bytes of the plan for R requests.
+constexpr int64_t kAttnPlanMaxSort = 4096;
+size_t attention_plan_bytes(int64_t R);
+hipError_t launch_attention_plan(const int32_t* cand_off, const int32_t* kv_off, int64_t R,
+                                 int q_len, int heads, int32_t* plan, hipStream_t s);
 // Grouping of a per-candidate map by request for the tiled attention kernel:
 // false when R or the per-block count table is too large for it (then the
 // general kernel runs); the workspace it needs, 0 in that case.

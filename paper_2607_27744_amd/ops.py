@@ -361,47 +361,95 @@ def dca_attention_residual(q, k, v, cand_offsets, kv_offsets, residual, *, scale
                       residual=residual, out_sum=out_sum)
 
 
-def dca_attention_proj(x, w_q, k, v, cand_offsets, kv_offsets, *, heads, residual=None,
-                       scale=None, out=None, out_sum=None, stream=None):
-    """DCA with the candidate queries projected in the kernel: q = x @ w_q^T viewed as
-    [N, T, heads, d] (x [N, T, d_in], w_q [heads * d, d_in]). Returns out, or
-    (out, out_sum) when `residual` is given (out_sum = round(out + residual))."""
+def dca_attention_plan_size(num_requests):
+    return int(_lib.load().rocs_dca_attention_plan_size(num_requests))
+
+
+def dca_attention_plan(cand_offsets, kv_offsets, *, num_cand, heads, q_len=1, plan=None,
+                       stream=None):
+    """rocs_dca_attention_plan: the tiled attention's tile order for these offsets
+    (longest history first), into `plan` (uint8 device tensor, allocated here when
+    not given). One plan serves every attention call over the same offsets."""
     lib = _lib.load()
-    _need(x.dim() == 3 and x.is_contiguous(), "x must be a contiguous [N, T, d_in] tensor")
-    n_cand, q_len, d_in = x.shape
-    _need(w_q.dim() == 2 and w_q.is_contiguous() and w_q.shape[1] == d_in
-          and w_q.shape[0] % heads == 0, "w_q must be a contiguous [heads * d, d_in] tensor")
-    dim = w_q.shape[0] // heads
+    n_req = kv_offsets.numel() - 1
+    _offsets(kv_offsets, n_req)
+    _offsets(cand_offsets, n_req)
+    need = dca_attention_plan_size(n_req)
+    if plan is None:
+        plan = torch.empty(need, dtype=torch.uint8, device=kv_offsets.device)
+    _need(plan.dtype == torch.uint8 and plan.is_contiguous() and plan.numel() >= need,
+          f"plan must be a contiguous uint8 tensor of at least {need} bytes")
+    _on_gpu(cand_offsets, kv_offsets, plan)
+    _lib.check(lib.rocs_dca_attention_plan(_ptr(cand_offsets), _ptr(kv_offsets), n_req,
+                                           num_cand, q_len, heads, _ptr(plan), plan.numel(),
+                                           _stream(stream)), "rocs_dca_attention_plan")
+    return plan
+
+
+def dca_attention_ex(q, k, v, cand_offsets, kv_offsets, *, w_q=None, heads=None, plan=None,
+                     residual=None, scale=None, out=None, out_sum=None, stream=None):
+    """rocs_dca_attention_ex. Without w_q, q is the query [N, T, H, d]; with w_q
+    [heads * d, d_in], q holds x [N, T, d_in] and the kernel projects it
+    (q = x @ w_q^T viewed as [N, T, heads, d]). `plan` (from dca_attention_plan)
+    orders the tiles. Returns out, or (out, out_sum) when `residual` is given
+    (out_sum = round(out + residual))."""
+    lib = _lib.load()
+    if w_q is None:
+        _need(q.dim() == 4 and q.is_contiguous(), "q must be a contiguous [N, T, H, d] tensor")
+        n_cand, q_len, heads, dim = q.shape
+        d_in = 0
+    else:
+        _need(q.dim() == 3 and q.is_contiguous(), "x must be a contiguous [N, T, d_in] tensor")
+        _need(heads is not None, "heads is required with w_q")
+        n_cand, q_len, d_in = q.shape
+        _need(w_q.dim() == 2 and w_q.is_contiguous() and w_q.shape[1] == d_in
+              and w_q.shape[0] % heads == 0, "w_q must be a contiguous [heads * d, d_in] tensor")
+        _need(w_q.dtype == q.dtype, "x and w_q must share one dtype")
+        dim = w_q.shape[0] // heads
     _need(k.dim() == 3 and v.dim() == 3 and k.shape == v.shape and k.shape[1:] == (heads, dim),
           "k and v must be [L, heads, d]")
     _need(k.stride(2) == 1 and k.stride(1) == dim and v.stride(2) == 1 and v.stride(1) == dim,
           "k/v rows must be dense [H, d] blocks")
     _need(k.stride(0) == v.stride(0), "k and v must share a row stride")
-    for t in (w_q, k, v):
-        _need(t.dtype == x.dtype, "x, w_q, k, v must share one dtype")
+    for t in (k, v):
+        _need(t.dtype == q.dtype, "q (or x), k, v must share one dtype")
     n_req = kv_offsets.numel() - 1
     _offsets(kv_offsets, n_req)
     _offsets(cand_offsets, n_req)
     shape = (n_cand, q_len, heads, dim)
     if out is None:
-        out = torch.empty(shape, dtype=x.dtype, device=x.device)
-    _need(tuple(out.shape) == shape and out.dtype == x.dtype and out.is_contiguous(),
-          "out must be [N, T, heads, d] of x's dtype")
+        out = torch.empty(shape, dtype=q.dtype, device=q.device)
+    _need(tuple(out.shape) == shape and out.dtype == q.dtype and out.is_contiguous(),
+          "out must be [N, T, heads, d] of q's dtype")
     if residual is not None:
-        _need(tuple(residual.shape) == shape and residual.dtype == x.dtype and
+        _need(tuple(residual.shape) == shape and residual.dtype == q.dtype and
               residual.is_contiguous(), "residual must be a contiguous [N, T, heads, d] tensor")
         if out_sum is None:
             out_sum = torch.empty_like(out)
         _need(out_sum.shape == out.shape and out_sum.dtype == out.dtype and
               out_sum.is_contiguous(), "out_sum must match out")
-    _on_gpu(x, w_q, k, v, cand_offsets, kv_offsets, out, residual, out_sum)
+    if plan is not None:
+        _need(plan.dtype == torch.uint8 and plan.is_contiguous(), "plan must be a uint8 tensor")
+    _on_gpu(q, w_q, k, v, cand_offsets, kv_offsets, out, residual, out_sum, plan)
     stride = k.stride(0) if k.shape[0] > 1 else heads * dim
-    _lib.check(lib.rocs_dca_attention_proj(
-        _ptr(x), d_in, _ptr(w_q), _ptr(k), _ptr(v), _ptr(cand_offsets), _ptr(kv_offsets), n_req,
-        n_cand, q_len, heads, dim, stride, float(scale or 0.0), _dtype_code(x),
-        _ptr(residual), _ptr(out), _ptr(out_sum) if residual is not None else None,
-        _stream(stream)), "rocs_dca_attention_proj")
+    _lib.check(lib.rocs_dca_attention_ex(
+        _ptr(q), d_in, _ptr(w_q), _ptr(k), _ptr(v), _ptr(cand_offsets), _ptr(kv_offsets),
+        _ptr(plan), plan.numel() if plan is not None else 0, n_req, n_cand, q_len, heads, dim,
+        stride, float(scale or 0.0), _dtype_code(q), _ptr(residual), _ptr(out),
+        _ptr(out_sum) if residual is not None else None, _stream(stream)),
+        "rocs_dca_attention_ex")
     return (out, out_sum) if residual is not None else out
+
+
+def dca_attention_proj(x, w_q, k, v, cand_offsets, kv_offsets, *, heads, residual=None,
+                       plan=None, scale=None, out=None, out_sum=None, stream=None):
+    """DCA with the candidate queries projected in the kernel: q = x @ w_q^T viewed as
+    [N, T, heads, d] (x [N, T, d_in], w_q [heads * d, d_in]). Returns out, or
+    (out, out_sum) when `residual` is given (out_sum = round(out + residual))."""
+    _need(w_q is not None, "w_q is required")
+    return dca_attention_ex(x, k, v, cand_offsets, kv_offsets, w_q=w_q, heads=heads, plan=plan,
+                            residual=residual, scale=scale, out=out, out_sum=out_sum,
+                            stream=stream)
 
 
 def dca_attention_mapped_workspace_size(num_requests, num_cand):

@@ -67,7 +67,10 @@ def prepare(w, device="cuda"):
         p.kv = torch.empty((l_tot, 4 * h * d), dtype=torch.bfloat16, device=dev)
         p.kv1, p.kv2 = p.kv[:, :2 * h * d], p.kv[:, 2 * h * d:]
         # The candidate query projections run inside the attention kernels
-        # (rocs_dca_attention_proj), so Q1 and Q2 never reach HBM.
+        # (rocs_dca_attention_ex with W_q), so Q1 and Q2 never reach HBM. Both
+        # layers share one tile plan (longest history first) per batch.
+        p.plan = torch.empty(ops.dca_attention_plan_size(w.n_req), dtype=torch.uint8,
+                             device=dev)
         p.a1 = torch.empty((w.n_cand, 1, h, d), dtype=torch.bfloat16, device=dev)
         p.a2 = torch.empty_like(p.a1)
         p.u = torch.empty_like(p.a1)      # layer-2 query input, round(A1 + e_c)
@@ -130,12 +133,15 @@ def step_calls(p):
         # pointwise residual u = A1 + e_c is formed in the layer-1 epilogue,
         # so layer 2 projects one tensor.
         return [lambda: ops.ikbo_linear(p.s, p.wkv, out=p.kv),
+                lambda: ops.dca_attention_plan(p.cand_offsets, p.kv_offsets, num_cand=n,
+                                               heads=p.h, plan=p.plan),
                 lambda: ops.dca_attention_proj(
                     p.e_c.view(n, 1, p.h * p.d), p.wq1, k1, v1, p.cand_offsets, p.kv_offsets,
-                    heads=p.h, residual=p.e_c.view(n, 1, p.h, p.d), out=p.a1, out_sum=p.u),
+                    heads=p.h, plan=p.plan, residual=p.e_c.view(n, 1, p.h, p.d), out=p.a1,
+                    out_sum=p.u),
                 lambda: ops.dca_attention_proj(p.u.view(n, 1, p.h * p.d), p.wq2, k2, v2,
                                                p.cand_offsets, p.kv_offsets, heads=p.h,
-                                               out=p.a2)]
+                                               plan=p.plan, out=p.a2)]
     if cid == 4:
         return [lambda: ops.glm_fm_linear(p.x_req, p.x_cand, p.cand_offsets, p.w_req,
                                           p.w_cand, activation="relu", out=p.out,

@@ -29,7 +29,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported_and_bound(lib):
     names = _declared()
-    assert len(names) == 24
+    assert len(names) == 26
     assert sorted(_lib.SIGNATURES) == names
     for n in names:
         assert hasattr(lib, n)
@@ -124,14 +124,13 @@ def test_attention_residual_argument_errors(lib):
 
 
 @no_gpu
-def test_attention_proj_argument_errors(lib):
+def test_attention_ex_argument_errors(lib):
     def call(**kw):
         a = dict(x=FAKE[0], d_in=256, wq=FAKE[8], k=FAKE[1], v=FAKE[2], co=FAKE[3], ko=FAKE[4],
-                 R=2, N=4, T=1, H=2, d=64, stride=0, scale=0.0, dtype=1, res=None, out=FAKE[5],
-                 out_sum=None, stream=None)
+                 plan=None, plan_bytes=0, R=2, N=4, T=1, H=2, d=64, stride=0, scale=0.0,
+                 dtype=1, res=None, out=FAKE[5], out_sum=None, stream=None)
         a.update(kw)
-        return lib.rocs_dca_attention_proj(*a.values())
-    assert call(wq=None) == _lib.INVALID_ARGUMENT
+        return lib.rocs_dca_attention_ex(*a.values())
     assert call(d_in=0) == _lib.INVALID_ARGUMENT
     assert call(x=None) == _lib.INVALID_ARGUMENT
     assert call(out=FAKE[0]) == _lib.INVALID_ARGUMENT        # out aliases x
@@ -140,6 +139,36 @@ def test_attention_proj_argument_errors(lib):
     assert call(res=FAKE[6], out_sum=FAKE[0]) == _lib.INVALID_ARGUMENT   # out_sum aliases x
     assert call(d=300) == _lib.UNSUPPORTED
     assert call(N=0) == _lib.OK
+    assert call(wq=None, d_in=0, N=0) == _lib.OK              # plain query form
+    # The plan: at least rocs_dca_attention_plan_size(R) bytes, clear of the outputs.
+    need = lib.rocs_dca_attention_plan_size(2)
+    assert need >= (8 + 2 * 2 + 1) * 4 and need % 256 == 0
+    assert call(plan=FAKE[9], plan_bytes=need - 4) == _lib.WORKSPACE_TOO_SMALL
+    assert call(plan=FAKE[5], plan_bytes=need) == _lib.INVALID_ARGUMENT   # plan aliases out
+    assert call(plan=P(0x90002), plan_bytes=need) == _lib.INVALID_ARGUMENT   # misaligned
+    assert call(plan=FAKE[9], plan_bytes=need, N=0) == _lib.OK
+
+
+@no_gpu
+def test_attention_plan_argument_errors(lib):
+    assert lib.rocs_dca_attention_plan_size(-1) == 0
+    assert lib.rocs_dca_attention_plan_size(1 << 31) == 0
+    assert lib.rocs_dca_attention_plan_size(0) == 256
+
+    def call(**kw):
+        a = dict(co=FAKE[3], ko=FAKE[4], R=2, N=4, T=1, H=2, plan=FAKE[9], plan_bytes=1 << 12,
+                 stream=None)
+        a.update(kw)
+        return lib.rocs_dca_attention_plan(*a.values())
+    assert call(plan=None) == _lib.INVALID_ARGUMENT
+    assert call(co=None) == _lib.INVALID_ARGUMENT
+    assert call(T=0) == _lib.INVALID_ARGUMENT
+    assert call(H=0) == _lib.INVALID_ARGUMENT
+    assert call(R=-1) == _lib.INVALID_ARGUMENT
+    assert call(plan_bytes=16) == _lib.WORKSPACE_TOO_SMALL
+    assert call(plan=P(0x90002)) == _lib.INVALID_ARGUMENT   # misaligned
+    assert call(plan=FAKE[3]) == _lib.INVALID_ARGUMENT      # plan overlaps the offsets
+    assert call(N=1 << 30, H=64) == _lib.UNSUPPORTED        # beyond the tile grid
 
 
 @no_gpu

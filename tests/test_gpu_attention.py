@@ -292,3 +292,88 @@ def test_attention_proj_general_kernel(gpu_lib, dim, d_in, bf16):
     assert_close(host(out), want, f"proj general d{dim} in{d_in}", **tol)
     want_sum = (out.float() + dev(res).float()).to(out.dtype)
     assert torch.equal(out_sum, want_sum)
+
+
+def _plan_want(co, ko, heads, q_len=1, rows=128):
+    """The tile plan the kernel order follows, from its definition: requests by
+    history length, longest first (lengths from 2^20 - 1 on count as equal;
+    ties by index), and the running sum of heads * ceil(n_r q_len / rows) in
+    that order."""
+    co, ko = np.asarray(co, np.int64), np.asarray(ko, np.int64)
+    lens = np.minimum(np.diff(ko), (1 << 20) - 1)
+    order = sorted(range(lens.size), key=lambda r: (-lens[r], r))
+    tiles = [heads * -(-(int(co[r + 1] - co[r]) * q_len) // rows) for r in order]
+    return np.array(order, np.int64), np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
+
+
+@pytest.mark.parametrize("counts,lens", [
+    ([300, 1, 0, 211], [70, 5, 0, 129]),
+    ([5, 7, 9, 11, 13], [64, 64, 300, 64, 300]),          # ties keep index order
+    ([1], [1]),
+    (list(range(0, 3000, 3)), [(37 * r) % 1500 for r in range(1000)]),
+], ids=["ragged", "ties", "one", "r1000"])
+@pytest.mark.parametrize("heads,q_len", [(4, 1), (2, 3)])
+def test_attention_plan_contents(gpu_lib, counts, lens, heads, q_len):
+    co = wl.offsets_from_counts(np.asarray(counts))
+    ko = wl.offsets_from_counts(np.asarray(lens))
+    plan = ops.dca_attention_plan(dev_i32(co), dev_i32(ko), num_cand=int(co[-1]), heads=heads,
+                                  q_len=q_len)
+    torch.cuda.synchronize()
+    got = plan.view(torch.int32).cpu().numpy().astype(np.int64)
+    r = len(counts)
+    order, pref = _plan_want(co, ko, heads, q_len)
+    assert got[0] == 1 and got[1] == pref[-1] and got[2] == r and got[3] == heads
+    assert got[4] == q_len and got[5] == 128
+    np.testing.assert_array_equal(got[8:8 + r], order)
+    np.testing.assert_array_equal(got[8 + r:8 + 2 * r + 1], pref)
+
+
+def test_attention_plan_beyond_the_sort_keeps_the_builtin_order(gpu_lib):
+    # 5000 requests: the plan records mode 0 and the kernel's own order runs.
+    rng = np.random.default_rng(5)
+    counts, lens = rng.integers(0, 40, 5000), rng.integers(0, 90, 5000)
+    case = wl.attention_case(counts, lens, 2, 64, seed=3)
+    args = (dev_bf16(case.k), dev_bf16(case.v), dev_i32(case.cand_offsets),
+            dev_i32(case.kv_offsets))
+    plan = ops.dca_attention_plan(args[2], args[3], num_cand=case.n_cand, heads=2)
+    torch.cuda.synchronize()
+    head = plan.view(torch.int32)[:8].cpu().numpy()
+    assert head[0] == 0 and head[2] == 5000
+    q = dev_bf16(case.q)
+    torch.testing.assert_close(ops.dca_attention_ex(q, *args, plan=plan),
+                               ops.dca_attention(q, *args), rtol=0, atol=0)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"n{sum(s[0])}-L{sum(s[1])}")
+@pytest.mark.parametrize("head_dim,q_len", [(64, 1), (128, 1), (64, 3)])
+def test_attention_with_plan_is_bit_identical(gpu_lib, shape, head_dim, q_len):
+    # The plan only reorders whole tiles: every output bit is the same, and a
+    # plan made for other heads or q_len is ignored.
+    counts, lens = shape
+    case = wl.attention_case(counts, lens, 2, head_dim, q_len=q_len, seed=7)
+    q = dev_bf16(case.q)
+    args = (dev_bf16(case.k), dev_bf16(case.v), dev_i32(case.cand_offsets),
+            dev_i32(case.kv_offsets))
+    ref = ops.dca_attention(q, *args)
+    plan = ops.dca_attention_plan(args[2], args[3], num_cand=case.n_cand, heads=2, q_len=q_len)
+    other = ops.dca_attention_plan(args[2], args[3], num_cand=case.n_cand, heads=3, q_len=q_len)
+    got = ops.dca_attention_ex(q, *args, plan=plan)
+    got_other = ops.dca_attention_ex(q, *args, plan=other)
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref)
+    assert torch.equal(got_other, ref)
+    assert_close(host(got), _want(case), f"planned {shape} d{head_dim} T{q_len}")
+
+
+def test_attention_proj_with_plan(gpu_lib):
+    case, x, wq, res, want = _proj_case([300, 1, 0, 211, 40], [70, 5, 0, 129, 1000], 4, 64, 256,
+                                        seed=23)
+    X, WQ, RES = dev_bf16(x), dev_bf16(wq), dev_bf16(res)
+    args = (dev_bf16(case.k), dev_bf16(case.v), dev_i32(case.cand_offsets),
+            dev_i32(case.kv_offsets))
+    plan = ops.dca_attention_plan(args[2], args[3], num_cand=case.n_cand, heads=4)
+    ref_out, ref_sum = ops.dca_attention_proj(X, WQ, *args, heads=4, residual=RES)
+    out, out_sum = ops.dca_attention_proj(X, WQ, *args, heads=4, residual=RES, plan=plan)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref_out) and torch.equal(out_sum, ref_sum)
+    assert_close(host(out), want, "proj planned")
