@@ -254,26 +254,41 @@ def main():
         pipelines.step(p)
     torch.cuda.synchronize()
 
+    # The timed steps carry no per-operator events (each event pair between
+    # two launches adds a gap); the per-operator times come from a second
+    # pass of the same number of steps, bracketed per operator.
     log(f"timing x{args.steps}" + (" (512 MiB written between steps)" if flush else ""))
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in fns] for _ in range(args.steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
         if flush:
             scratch.fill_(s & 0xff)       # evicts the previous step's data; outside the events
-        for i, fn in enumerate(fns):
-            ev[s][i][0].record(stream)
+        ev[s][0].record(stream)
+        for fn in fns:
             fn()
-            ev[s][i][1].record(stream)
+        ev[s][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    step_ms = [ev[s][0][0].elapsed_time(ev[s][-1][1]) for s in range(args.steps)]
+    step_ms = [ev[s][0].elapsed_time(ev[s][1]) for s in range(args.steps)]
     # Back-to-back steps: the wall clock over the K steps. With the flush
     # between steps the wall clock includes it, so the step time is the
     # median of the per-step event times instead.
     ms_step = float(np.median(step_ms)) if flush else 1e3 * wall / args.steps
-    op_ms = [float(np.median([ev[s][i][0].elapsed_time(ev[s][i][1])
+
+    log(f"per-operator pass x{args.steps}")
+    op_ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in fns] for _ in range(args.steps)]
+    for s in range(args.steps):
+        if flush:
+            scratch.fill_(s & 0xff)
+        for i, fn in enumerate(fns):
+            op_ev[s][i][0].record(stream)
+            fn()
+            op_ev[s][i][1].record(stream)
+    torch.cuda.synchronize()
+    op_ms = [float(np.median([op_ev[s][i][0].elapsed_time(op_ev[s][i][1])
                               for s in range(args.steps)])) for i in range(len(fns))]
 
     kernels = {}
@@ -314,7 +329,8 @@ def main():
                    "wall_ms_per_step": round(1e3 * wall / args.steps, 4),
                    "cache_flush_between_steps": flush,
                    "step_time": "median of per-step HIP events" if flush
-                   else "wall clock over the timed steps"},
+                   else "wall clock over the timed steps",
+                   "per_operator": "medians of per-operator HIP events in a second pass"},
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32" if fp32 else "bf16", "data": "synthetic",
         "config": {"workload": f"{names[args.workload]}: {wl.WORKLOAD_NAMES[args.workload]}",
