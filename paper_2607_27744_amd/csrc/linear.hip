@@ -317,6 +317,7 @@ void ikbo_gemm_bf16(
 // Rows past the tile's end are clamped loads whose results are not stored.
 // ---------------------------------------------------------------------------
 constexpr int kStreamBM = 256, kStreamBN = 256, kStreamBK = 64;
+constexpr int kCpolNT = 2;   // buffer-instruction cache policy bits: NT (the former SLC bit)
 
 // ReLU of two packed bf16 values: as 16-bit integers the negative values
 // (sign bit set) are exactly those below zero, so a packed integer max with
@@ -728,8 +729,11 @@ void ikbo_gemm_stream(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w
         for (int i = 0; i < 4; ++i) {
           const int r = 8 * i + rr;
           const u32x4 v = *reinterpret_cast<const ROCS_LDS u32x4*>(st + r * 128 + 16 * (cr ^ (r & 7)));
+          // Non-temporal (cache policy NT): the output is not read again by
+          // this kernel, so it should not push the candidate slabs and the
+          // weights out of L2 before the tile's other feature tiles read them.
           __builtin_amdgcn_raw_buffer_store_b128(
-              v, ro, vo + 2u * (uint32_t)(32 * fn + 8 * i) * (uint32_t)D, 0, 0);
+              v, ro, vo + 2u * (uint32_t)(32 * fn + 8 * i) * (uint32_t)D, 0, kCpolNT);
         }
       }
       return;
