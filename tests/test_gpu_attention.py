@@ -306,12 +306,21 @@ def _plan_want(co, ko, heads, q_len=1, rows=128):
     return np.array(order, np.int64), np.concatenate([[0], np.cumsum(tiles)]).astype(np.int64)
 
 
+def _many(r, seed):
+    rng = np.random.default_rng(seed)
+    return rng.integers(0, 300, r).tolist(), rng.integers(0, 2000, r).tolist()
+
+
 @pytest.mark.parametrize("counts,lens", [
     ([300, 1, 0, 211], [70, 5, 0, 129]),
     ([5, 7, 9, 11, 13], [64, 64, 300, 64, 300]),          # ties keep index order
     ([1], [1]),
+    ([40, 0, 7], [0, 0, 0]),                              # every history empty
+    _many(256, 1),                                        # largest counted ranking
+    _many(257, 2),                                        # smallest bitonic sort
     (list(range(0, 3000, 3)), [(37 * r) % 1500 for r in range(1000)]),
-], ids=["ragged", "ties", "one", "r1000"])
+    _many(4096, 3),                                       # largest sorted plan
+], ids=["ragged", "ties", "one", "empty-histories", "r256", "r257", "r1000", "r4096"])
 @pytest.mark.parametrize("heads,q_len", [(4, 1), (2, 3)])
 def test_attention_plan_contents(gpu_lib, counts, lens, heads, q_len):
     co = wl.offsets_from_counts(np.asarray(counts))
@@ -363,6 +372,25 @@ def test_attention_with_plan_is_bit_identical(gpu_lib, shape, head_dim, q_len):
     assert torch.equal(got, ref)
     assert torch.equal(got_other, ref)
     assert_close(host(got), _want(case), f"planned {shape} d{head_dim} T{q_len}")
+
+
+@pytest.mark.parametrize("q_len", [1, 3])
+def test_attention_ex_all_options(gpu_lib, q_len):
+    # Projection, residual and plan together, several query tokens: equal to
+    # the three-call composition (project, attend, add) bit for bit.
+    case, x, wq, res, want = _proj_case([129, 0, 300, 1, 64], [700, 9, 0, 64, 1], 4, 64, 256,
+                                        seed=31, q_len=q_len)
+    X, WQ, RES = dev_bf16(x), dev_bf16(wq), dev_bf16(res)
+    args = (dev_bf16(case.k), dev_bf16(case.v), dev_i32(case.cand_offsets),
+            dev_i32(case.kv_offsets))
+    plan = ops.dca_attention_plan(args[2], args[3], num_cand=case.n_cand, heads=4, q_len=q_len)
+    out, out_sum = ops.dca_attention_ex(X, *args, w_q=WQ, heads=4, plan=plan, residual=RES)
+    q = ops.ikbo_linear(X.view(-1, 256), WQ).view(-1, q_len, 4, 64)
+    ref = ops.dca_attention(q, *args)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    assert torch.equal(out_sum, (ref.float() + RES.float()).to(torch.bfloat16))
+    assert_close(host(out), want, f"ex T{q_len}")
 
 
 def test_attention_proj_with_plan(gpu_lib):
