@@ -17,8 +17,10 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import assert_close, host, tile_rows
+from gpu_util import ATOL, assert_close, host, tile_rows
+from oracle import ikbo
 from oracle import pipelines as oracle_pipelines
+from oracle.bf16 import round_bf16
 from paper_2607_27744_amd import pipelines, workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -106,3 +108,49 @@ def test_workload5_production_retrieval(gpu_lib):
     # Properties that hold at any size, checked on every candidate.
     assert bool(torch.isfinite(got["attention"]).all()) and bool(torch.isfinite(got["out2"]).all())
     assert bool((got["h1"] >= 0).all())
+
+
+def _fm_flip_bound(w):
+    """Largest change of the workload 4 output that the bf16 rounding of Y can
+    cause between the GPU (fp32 accumulation) and the oracle (fp64).
+
+    Products of bf16 values are exact in fp32, so the GPU's Y element is within
+    gamma = E * 2^-24 * sum_k |x_ik x_jk| of the exact one (E = 128 terms, any
+    summation order). Where a bf16 rounding boundary lies inside that interval
+    the two sides may round Y to neighbouring values, one bf16 step apart; the
+    next layer scales each such step by |W|. Elements with no boundary within
+    gamma contribute nothing: everywhere else the strict tolerance holds."""
+    y_r, y_c = ikbo.glm_fm(w.x_req, w.x_cand, w.cand_offsets)
+    a_r, a_c = ikbo.glm_fm(np.abs(w.x_req), np.abs(w.x_cand), w.cand_offsets)
+    emb = w.x_req.shape[-1]
+
+    def step(y, a):
+        g = emb * 2.0 ** -24 * a
+        return np.abs(round_bf16(y + g) - round_bf16(y - g))
+
+    req = ikbo.request_ids(w.cand_offsets)
+    return step(y_c, a_c) @ np.abs(w.w_cand).T + (step(y_r, a_r) @ np.abs(w.w_req).T)[req]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("cid,fn,keys", [
+    (2, oracle_pipelines.retrieval_mlp, ("out",)),
+    (3, oracle_pipelines.ranking_dca, ("a1", "u", "a2")),
+    (4, oracle_pipelines.fm_linear, ("y_req", "out")),
+], ids=["workload2", "workload3", "workload4"])
+def test_workload_every_row(gpu_lib, cid, fn, keys):
+    # Every candidate row at the full size (the oracle takes about 20 s per
+    # workload on the host), beyond the one-row-per-tile sample above. At
+    # workload 4 the output may also move by the bf16 steps of Y that the two
+    # accumulation precisions can round apart (_fm_flip_bound).
+    w = wl.make_workload(cid)
+    got = _gpu(w)
+    _say(f"oracle on all {w.n_cand} rows")
+    want = fn(w)
+    for key in keys:
+        atol = ATOL
+        if cid == 4 and key == "out":
+            bound = _fm_flip_bound(w)
+            atol = ATOL + bound
+            _say(f"rows with a possible Y rounding step: {int((bound.max(axis=1) > 0).sum())}")
+        assert_close(host(got[key]), want[key], f"{key} (all rows)", atol=atol)
