@@ -122,7 +122,8 @@ constexpr int kProjIn = 256;   // input width of the fused query projection
 // Tile plan (launch_attention_plan): an int32 array. Header: mode (1 =
 // sorted, 0 = use the built-in order), T (tiles over all heads), R, H, T_q,
 // rows per tile; then from kPlanHeader the request ids sorted by history
-// length, longest first (ties by id), and their tile offsets P[0..R]
+// length, longest first (lengths from 2^20 - 1 on count as equal; ties by
+// id), and their tile offsets P[0..R]
 // (P[i+1] - P[i] = H * ceil(n_r T_q / rows per tile) for the i-th request r;
 // all heads of one request are consecutive, each head's tiles in order).
 // Workgroup b takes tile t of that list, in chunks of kPlanChunk consecutive
