@@ -316,11 +316,12 @@ def _many(r, seed):
     ([5, 7, 9, 11, 13], [64, 64, 300, 64, 300]),          # ties keep index order
     ([1], [1]),
     ([40, 0, 7], [0, 0, 0]),                              # every history empty
+    ([], []),                                             # no requests
     _many(256, 1),                                        # largest counted ranking
     _many(257, 2),                                        # smallest bitonic sort
     (list(range(0, 3000, 3)), [(37 * r) % 1500 for r in range(1000)]),
     _many(4096, 3),                                       # largest sorted plan
-], ids=["ragged", "ties", "one", "empty-histories", "r256", "r257", "r1000", "r4096"])
+], ids=["ragged", "ties", "one", "empty-histories", "none", "r256", "r257", "r1000", "r4096"])
 @pytest.mark.parametrize("heads,q_len", [(4, 1), (2, 3)])
 def test_attention_plan_contents(gpu_lib, counts, lens, heads, q_len):
     co = wl.offsets_from_counts(np.asarray(counts))
