@@ -74,18 +74,21 @@ def stats(path):
 
 
 def trace(path):
-    """Per-launch-shape durations from a --kernel-trace CSV (kernel, grid)."""
+    """Per-launch-shape durations from a --kernel-trace CSV (kernel, grid):
+    mean and median (the median leaves out the slower first launches)."""
     import collections
+    import statistics
     groups = collections.OrderedDict()
     for r in _rows(path, "*kernel_trace.csv"):
         grid = r.get("Grid_Size_X") or r.get("Grid_Size") or "?"
         key = (r["Kernel_Name"][:60], grid)
         groups.setdefault(key, []).append(
             (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e6)
-    print("| kernel | grid (work-items) | launches | avg ms |")
-    print("|---|---|---|---|")
+    print("| kernel | grid (work-items) | launches | avg ms | median ms |")
+    print("|---|---|---|---|---|")
     for (name, grid), v in groups.items():
-        print(f"| {name} | {grid} | {len(v)} | {sum(v) / len(v):.4f} |")
+        print(f"| {name} | {grid} | {len(v)} | {sum(v) / len(v):.4f} | "
+              f"{statistics.median(v):.4f} |")
 
 
 def traffic(fetch_dir, write_dir, copy_fetch, copy_write, substring, name):
